@@ -1,0 +1,287 @@
+"""Benchmark of one hybrid-batch decoder-layer iteration on one MI355X.
+
+A step is one hb_run_iteration over the Llama-3-8B-shaped layer with one
+512-token prefill chunk (offset drawn from 0..4096) plus 64 decodes (contexts
+512..4096) over a 2M-token paged KV cache, inputs already resident in HBM.
+Prints one JSON line: new tokens/s, per-step latency, the roofline of the
+dominant kernel, the CPU oracle's rate on the same batch and the latency
+profile against chunk size that dynamic chunking consumes.
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 10]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM = 8.0e12       # MI355X HBM3E bytes/s
+PEAK_BF16 = 2.5e15      # MI355X dense bf16 MFMA flop/s
+RIDGE = PEAK_BF16 / PEAK_HBM
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_work(shape, requests, out_f32=True):
+    """Algorithmic (flops, HBM bytes) of each kernel for one iteration: the
+    operands each must read and the results it must write once, nothing more."""
+    T = sum(c for c, _ in requests)
+    H, nq, nkv, hd, F = shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn_dim
+    qd, qkv_n = nq * hd, (nq + 2 * nkv) * hd
+    pairs = sum(c * x + c * (c + 1) / 2 for c, x in requests)
+    kv_tok = sum(c + x for c, x in requests)
+    yb = 4 if out_f32 else 2
+    return {
+        "rmsnorm_attn": (4.0 * T * H, 2.0 * T * H + 2 * H + 2.0 * T * H),
+        "gemm_qkv": (2.0 * T * H * qkv_n, 2.0 * (H * qkv_n + T * H + T * qkv_n)),
+        "rope_kv": (6.0 * T * (nq + nkv) * hd, 2.0 * T * qkv_n + 2.0 * T * qd + 2.0 * T * 2 * nkv * hd),
+        "attention": (4.0 * nq * hd * pairs, 2.0 * 2 * nkv * hd * kv_tok + 2.0 * T * qd * 2),
+        "gemm_o": (2.0 * T * qd * H, 2.0 * H * qd + 2.0 * T * qd + 2.0 * T * H + 4.0 * T * H),
+        "rmsnorm_ffn": (4.0 * T * H, 4.0 * T * H + 2 * H + 2.0 * T * H),
+        "gemm_gate_up": (2.0 * T * H * 2 * F, 2.0 * 2 * F * H + 2.0 * T * H + 2.0 * T * F),
+        "gemm_down": (2.0 * T * F * H, 2.0 * H * F + 2.0 * T * F + 4.0 * T * H + yb * T * H),
+    }
+
+
+def layer_work(shape, requests, out_f32=True):
+    T = sum(c for c, _ in requests)
+    H, nq, nkv, hd, F = shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn_dim
+    p_lin = shape.linear_params
+    pairs = sum(c * x + c * (c + 1) / 2 for c, x in requests)
+    kv_tok = sum(c + x for c, x in requests)
+    flops = 2.0 * T * p_lin + 4.0 * nq * hd * pairs
+    bytes_ = 2.0 * p_lin + 4.0 * H + 2.0 * 2 * nkv * hd * (kv_tok + T) + 2.0 * T * H + (4 if out_f32 else 2) * T * H
+    return flops, bytes_
+
+
+def kernel_sources_digest(names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2503_22562_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+TRAFFIC_SOURCES = {
+    "attention": ["k_attention.hip", "hb_device.h", "hb_plan.h"],
+    "gemm_gate_up": ["k_gemm.hip", "hb_device.h"],
+    "gemm_down": ["k_gemm.hip", "hb_device.h"],
+    "gemm_qkv": ["k_gemm.hip", "hb_device.h"],
+    "gemm_o": ["k_gemm.hip", "hb_device.h"],
+}
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, only
+    if the kernel's sources are unchanged since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path) or kernel not in TRAFFIC_SOURCES:
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("sources_digest") != kernel_sources_digest(TRAFFIC_SOURCES[kernel]):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(batch, weights_bits, budget_s=20.0):
+    """The oracle (fp64 NumPy) on the same batch, host cores, timed."""
+    import oracle
+    shape = batch.shape
+    w64 = oracle.weights_to_f64(weights_bits)
+    x = oracle.bf16_bits_to_f64(batch.x_in())
+    prior = {r: tuple(oracle.bf16_bits_to_f64(a) for a in batch.prior_kv(r))
+             for r, q in enumerate(batch.requests) if q.context_len}
+    times = []
+    t_start = time.perf_counter()
+    while True:
+        cache = oracle.PagedKVCache(batch.num_blocks, shape.n_kv_heads, shape.head_dim)
+        for r, (k, v) in prior.items():
+            cache.write(batch.requests[r].block_table, 0, k, v)
+        t0 = time.perf_counter()
+        oracle.layer_forward(w64, shape, cache, batch.requests, x)
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() - t_start > budget_s or len(times) >= 3:
+            break
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max(int(i.get("num_threads", 0)) for i in threadpool_info()) or threads
+    except Exception:
+        pass
+    t = float(np.median(times))
+    return {"value": batch.n_tokens / t, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"whole batch ({batch.n_tokens} tokens, {len(batch.requests)} requests), fp64 NumPy oracle, "
+                      f"median of {len(times)} runs of {t:.2f} s; cached-context seeding not timed"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true")
+    ap.add_argument("--profile-iters", type=int, default=15)
+    a = ap.parse_args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the hybrid-batch layer runs on a single MI355X; "
+              "run it with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import torch
+    from hb_workloads import LLAMA3_8B, POOL_TOKENS, SWEEP_CHUNKS, SWEEP_DECODES, llama8b_batch, make_weights, \
+        sweep_decode_contexts
+    from paper_2503_22562_amd import hb
+    from paper_2503_22562_amd.harness import DeviceLayer, to_device_bf16
+
+    torch.cuda.set_device(0)
+    shape = LLAMA3_8B
+    batch = llama8b_batch()
+    reqs = [(q.chunk_len, q.context_len, q.block_table) for q in batch.requests]
+    T = batch.n_tokens
+    log(f"bench: {batch.label}, T={T}; generating weights and cached context")
+    w = make_weights(shape)
+    dl = DeviceLayer(shape, w, POOL_TOKENS // 16, 4096, 512, pool_fill_bits=0)
+    for r, q in enumerate(batch.requests):
+        if q.context_len:
+            k, v = batch.prior_kv(r)
+            dl.append_kv(q.block_table, 0, k, v)
+    x = to_device_bf16(batch.x_in())
+    y = torch.empty((T, shape.hidden), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    log(f"bench: warmup {a.warmup}")
+    for _ in range(a.warmup):
+        dl.run(reqs, x, hb.HB_OUT_F32, y)
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` iterations, per-kernel HIP events on the layer's stream
+    hb.hb_set_kernel_timing(dl.layer, True)
+    hb.hb_kernel_times(dl.layer, reset=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        dl.run(reqs, x, hb.HB_OUT_F32, y)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ktimes = hb.hb_kernel_times(dl.layer, reset=True)
+    hb.hb_set_kernel_timing(dl.layer, False)
+    ms_per_step = wall * 1e3 / a.steps
+    log(f"bench: {ms_per_step:.4f} ms/step")
+
+    # same iteration without per-kernel events, and with the Infinity Cache flushed before each
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(a.steps)]
+    for i in range(a.steps):
+        flush.fill_(i & 0xFF)
+        ev[i][0].record(stream)
+        dl.run(reqs, x, hb.HB_OUT_F32, y)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    cold = sorted(s.elapsed_time(e) for s, e in ev)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(a.steps):
+        dl.run(reqs, x, hb.HB_OUT_F32, y)
+    torch.cuda.synchronize()
+    plain_ms = (time.perf_counter() - t1) * 1e3 / a.steps
+    del flush
+
+    work = kernel_work(shape, [(c, xx) for c, xx, _ in reqs])
+    kernels = {}
+    for name, (tot, n) in ktimes.items():
+        if n == 0:
+            continue
+        avg_ms = tot / n
+        fl, by = work.get(name, (0.0, 0.0))
+        kernels[name] = {"avg_ms": round(avg_ms, 5), "launches": n,
+                         "tflops": round(fl / (avg_ms * 1e-3) / 1e12, 2) if fl else None,
+                         "gbps": round(by / (avg_ms * 1e-3) / 1e9, 1) if by else None}
+    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
+    fl, by = work[dom]
+    avg_s = kernels[dom]["avg_ms"] * 1e-3
+    if fl / by > RIDGE:
+        roof = {"bound": "mfma", "achieved": round(fl / avg_s / 1e12, 2), "peak": PEAK_BF16 / 1e12,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(by / avg_s / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["kernel"] = dom
+    roof["algorithmic_flops"] = fl
+    roof["algorithmic_bytes"] = by
+    tr = measured_traffic(dom, "llama3-8b")
+    roof["traffic"] = tr
+    flops, bytes_ = layer_work(shape, [(c, xx) for c, xx, _ in reqs])
+    step_s = ms_per_step * 1e-3
+
+    profile = None
+    if not a.no_profile:
+        log("bench: latency profile (chunk x decode grid)")
+        mixes = [(sweep_decode_contexts(n), 0) for n in SWEEP_DECODES]
+        prof = hb.hb_profile(dl.layer, SWEEP_CHUNKS, mixes, warmup=3, iters=a.profile_iters, seed=1)
+        med = prof["median_ms"]
+        mono = all(med[i, j] * (1.01 if (n == 0 and SWEEP_CHUNKS[j] <= 256) else 1.0) >= med[i, j - 1]
+                   for i, n in enumerate(SWEEP_DECODES) for j in range(1, len(SWEEP_CHUNKS)))
+        profile = {"chunks": list(SWEEP_CHUNKS), "decodes": list(SWEEP_DECODES),
+                   "median_ms": np.round(med, 4).tolist(), "p90_ms": np.round(prof["p90_ms"], 4).tolist(),
+                   "tokens_per_s": np.round(prof["tokens_per_s"]).tolist(),
+                   "hbm_frac": np.round(prof["hbm_frac"], 3).tolist(),
+                   "mfma_frac": np.round(prof["mfma_frac"], 3).tolist(),
+                   "monotone_in_chunk": bool(mono), "cache": "512 MiB flush before each timed iteration"}
+
+    cpu = None
+    if not a.no_cpu_baseline:
+        log("bench: CPU oracle baseline")
+        del dl
+        torch.cuda.empty_cache()
+        cpu = cpu_baseline(batch, w)
+
+    out = {
+        "metric": "hybrid-batch layer throughput (new tokens/s) and latency",
+        "value": round(T / step_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights, N(0,1) activations and cached K/V)",
+        "config": {"workload": "llama3-8b layer: 1 prefill chunk of 512 at offset U{0..4096} + 64 decodes, "
+                               "contexts U{512..4096}, 2M-token paged pool", "tokens_per_step": T,
+                   "requests": len(reqs), "hidden": shape.hidden, "q_heads": shape.n_q_heads,
+                   "kv_heads": shape.n_kv_heads, "head_dim": shape.head_dim, "ffn": shape.ffn_dim,
+                   "kv_block": 16, "parallelism": "none (1 GPU)"},
+        "latency_ms": {"timed_region_per_step": round(ms_per_step, 5),
+                       "no_kernel_events": round(plain_ms, 5),
+                       "cache_flushed_median": round(cold[len(cold) // 2], 5),
+                       "cache_flushed_p10": round(cold[len(cold) // 10], 5),
+                       "cache_flushed_p90": round(cold[(9 * len(cold)) // 10], 5)},
+        "layer_roofline": {"algorithmic_gflop": round(flops / 1e9, 2), "algorithmic_mb": round(bytes_ / 1e6, 1),
+                           "mfma_frac": round(flops / step_s / PEAK_BF16, 4),
+                           "hbm_frac": round(bytes_ / step_s / PEAK_HBM, 4),
+                           "roofline_time_us": round(max(flops / PEAK_BF16, bytes_ / PEAK_HBM) * 1e6, 1)},
+        "roofline": roof,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+        "latency_profile": profile,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

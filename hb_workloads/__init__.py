@@ -18,6 +18,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import os
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -73,11 +74,42 @@ def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
     return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
-def _normal_bf16(rng: np.random.Generator, shape, std: float = 1.0) -> np.ndarray:
-    a = rng.standard_normal(size=shape, dtype=np.float32)
-    if std != 1.0:
-        a *= np.float32(std)
-    return f32_to_bf16_bits(a)
+_CHUNK = 1 << 18  # values per independent PCG64 stream
+_POOL = None
+
+
+def _pool():
+    global _POOL
+    if _POOL is None:
+        import concurrent.futures as cf
+        _POOL = cf.ThreadPoolExecutor(max_workers=max(1, min(16, os.cpu_count() or 1)))
+    return _POOL
+
+
+def _round_bf16(a: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bits, nearest-even (torch's cast, multi-threaded; the same
+    bits as f32_to_bf16_bits)."""
+    import torch
+    return torch.from_numpy(a).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def normal_bf16(key, shape, std: float = 1.0) -> np.ndarray:
+    """N(0, std^2) draws as bf16 bits. Chunk i of 2^18 values comes from its
+    own stream default_rng([*key, i]), so the values depend only on key and
+    shape, not on the number of threads."""
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.float32)
+    key = list(key)
+
+    def fill(i):
+        s = i * _CHUNK
+        e = min(n, s + _CHUNK)
+        np.random.default_rng(key + [i]).standard_normal(size=e - s, dtype=np.float32, out=out[s:e])
+        if std != 1.0:
+            out[s:e] *= np.float32(std)
+
+    list(_pool().map(fill, range((n + _CHUNK - 1) // _CHUNK)))
+    return _round_bf16(out).reshape(shape)
 
 
 # ----------------------------------------------------------------------------
@@ -107,7 +139,7 @@ def make_weights(shape: LayerShape, seed: Optional[int] = None) -> Dict[str, np.
     }
     out: Dict[str, np.ndarray] = {}
     for i, (name, (shp, std)) in enumerate(specs.items()):
-        out[name] = _normal_bf16(np.random.default_rng([seed, i]), shp, std)
+        out[name] = normal_bf16([seed, i], shp, std)
     for i, name in enumerate(("g_attn", "g_ffn")):
         rng = np.random.default_rng([seed, 10 + i])
         g = 1.0 + 0.1 * rng.standard_normal(size=(h,), dtype=np.float32)
@@ -150,16 +182,14 @@ class Batch:
 
     def x_in(self) -> np.ndarray:
         """Token activations ~ N(0,1), bf16 bits [T][hidden]."""
-        rng = np.random.default_rng([self.seed, 1])
-        return _normal_bf16(rng, (self.n_tokens, self.shape.hidden))
+        return normal_bf16([self.seed, 1], (self.n_tokens, self.shape.hidden))
 
     def prior_kv(self, r: int) -> Tuple[np.ndarray, np.ndarray]:
         """Synthetic cached K (already rotated) and V for positions [0, ctx) of
         request r, each ~ N(0,1), bf16 bits [ctx][n_kv][head_dim]."""
         req = self.requests[r]
         shp = (req.context_len, self.shape.n_kv_heads, self.shape.head_dim)
-        rng = np.random.default_rng([self.seed, 2, r])
-        return _normal_bf16(rng, shp), _normal_bf16(rng, shp)
+        return normal_bf16([self.seed, 2, r, 0], shp), normal_bf16([self.seed, 2, r, 1], shp)
 
 
 def blocks_needed(kv_len: int, block: int = KV_BLOCK) -> int:

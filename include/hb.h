@@ -1,0 +1,218 @@
+/*
+ * hb.h -- C ABI of the hybrid-batch decoder-layer library (libhb.so, gfx950).
+ *
+ * One call of hb_run_iteration executes one scheduler iteration of the kind
+ * described in Section 3.1 (steps 5 and 6) and Section 3.3 of the Niyama
+ * paper (arXiv 2503.22562): a single forward pass of one decoder layer over a
+ * mixed batch that holds every decoding request (one new token each) and
+ * prefill chunks whose length the dynamic-chunking policy chose. All linear
+ * layers run once over the concatenated tokens (the fused prefill-decode MLP
+ * of Section 3.3); attention reads each request's cached keys and values
+ * through a paged KV cache (PagedAttention, Section 3.6). hb_profile measures
+ * the latency of such iterations against chunk size and decode load, the
+ * offline profile that the chunk-size predictor of Section 3.6 is trained on.
+ *
+ * The layer is the Llama-3 pre-norm decoder layer (the paper evaluates
+ * Llama3-8B, evaluation setup): RMSNorm -> QKV projection -> rotate-half RoPE
+ * -> causal GQA attention over the paged cache -> O projection + residual ->
+ * RMSNorm -> SwiGLU FFN + residual. No biases.
+ *
+ * Conventions for every entry point:
+ *  - Device pointers are HIP device memory on the device that was current
+ *    when the layer was created; host pointers are ordinary host memory.
+ *  - bf16 is IEEE bfloat16 (uint16 bit patterns), fp32 is IEEE binary32.
+ *  - Every status other than HB_OK is returned before anything is enqueued,
+ *    so nothing on the device is modified; hb_last_error() then describes it.
+ *  - hb_run_iteration and hb_append_kv only enqueue work on the layer's
+ *    stream and return; the caller synchronises that stream before reading
+ *    results or reusing inputs. Host arrays passed to them (request tables,
+ *    block tables) are copied during the call and may be freed on return.
+ *  - A layer is used from one host thread at a time.
+ */
+#ifndef HB_H_
+#define HB_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HB_OK = 0,
+  HB_ERR_INVALID = 1,     /* malformed argument: null pointer, bad length, overlap */
+  HB_ERR_RANGE = 2,       /* a block id outside [0, num_blocks) */
+  HB_ERR_OOM = 3,         /* device or pinned host allocation failed */
+  HB_ERR_HIP = 4,         /* a HIP runtime call failed; hb_last_error() names it */
+  HB_ERR_UNSUPPORTED = 5  /* a shape the kernels do not implement */
+} hb_status;
+
+typedef struct hb_layer hb_layer; /* opaque, library-owned */
+
+/* Layer shape and capacity.
+ *   hidden        H, multiple of 64
+ *   n_q_heads     query heads; n_q_heads % n_kv_heads == 0 and the group
+ *                 size G = n_q_heads / n_kv_heads divides 16
+ *   n_kv_heads    key/value heads (GQA: q head h reads kv head h / G)
+ *   head_dim      64 or 128
+ *   ffn_dim       F, multiple of 16
+ *   kv_block_size must be 16 (tokens per paged block)
+ *   rope_theta    RoPE base; angle of pair j at position p is p*theta^(-2j/head_dim)
+ *   rms_eps       RMSNorm epsilon
+ *   max_batch_tokens  largest T = sum of chunk_len accepted by hb_run_iteration
+ *   max_requests      largest number of requests in one batch */
+typedef struct {
+  int32_t hidden, n_q_heads, n_kv_heads, head_dim, ffn_dim, kv_block_size;
+  float rope_theta, rms_eps;
+  int32_t max_batch_tokens, max_requests;
+} hb_layer_config;
+
+/* Layer weights: device bf16, row-major [out][in], caller-owned, must outlive
+ * the layer and stay unchanged while iterations run.
+ *   w_qkv      [(n_q + 2 n_kv) head_dim][H]; rows = [q heads | k heads | v heads]
+ *   w_o        [H][n_q head_dim]
+ *   w_gate_up  [2F][H]; rows = [gate (F rows) | up (F rows)]
+ *   w_down     [H][F]
+ *   g_attn, g_ffn  [H] RMSNorm gains */
+typedef struct {
+  const void *w_qkv, *w_o, *w_gate_up, *w_down, *g_attn, *g_ffn;
+} hb_layer_weights;
+
+/* Paged KV cache of one layer: device bf16, caller-owned.
+ *   k_pool  [num_blocks][n_kv_heads][16][head_dim]   (token-major in a block)
+ *   v_pool  [num_blocks][n_kv_heads][head_dim][16]   (dim-major in a block)
+ * Position p of a request lives in block block_table[p / 16], slot p % 16.
+ * Keys are stored after RoPE. */
+typedef struct {
+  void *k_pool, *v_pool;
+  int32_t num_blocks;
+} hb_kv_pool;
+
+/* Create a layer bound to weights, pool and a HIP stream (hipStream_t; NULL
+ * selects the null stream). Allocates the library's workspace for
+ * max_batch_tokens / max_requests on the current device.
+ * Errors: HB_ERR_INVALID (null pointer, non-positive size),
+ * HB_ERR_UNSUPPORTED (shape outside the limits above), HB_ERR_OOM, HB_ERR_HIP.
+ * On error *out is set to NULL. */
+hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w,
+                          const hb_kv_pool* pool, void* hip_stream, hb_layer** out);
+
+/* Free the workspace (after synchronising the layer's stream). NULL is a no-op. */
+void hb_destroy_layer(hb_layer* layer);
+
+/* Write already-rotated keys and values of one request into the paged cache
+ * (the cache of Section 3.6 that later iterations read).
+ *   block_table  host int32 [n_blocks], physical block ids of the request
+ *   context_len  position of the first token written
+ *   n_tokens     tokens written: positions [context_len, context_len + n_tokens)
+ *   k, v         device bf16 [n_tokens][n_kv_heads][head_dim]
+ * Only those slots change; every other byte of the pool is left untouched.
+ * Errors: HB_ERR_INVALID (null pointer, n_tokens < 0, context_len < 0,
+ * n_blocks < ceil((context_len + n_tokens) / 16)), HB_ERR_RANGE (a used block
+ * id outside [0, num_blocks)). n_tokens == 0 is a no-op. */
+hb_status hb_append_kv(hb_layer* layer, const int32_t* block_table, int32_t n_blocks,
+                       int32_t context_len, int32_t n_tokens, const void* k, const void* v);
+
+/* One request of a hybrid batch (Section 3.1, step 5). A decode has
+ * chunk_len == 1; a prefill chunk has chunk_len >= 1 new prompt tokens.
+ *   context_len  tokens of this request already in the cache; the new tokens
+ *                take positions [context_len, context_len + chunk_len) and
+ *                each attends to every earlier position and to itself
+ *   block_table  host int32 [n_blocks], n_blocks >= ceil((context_len + chunk_len) / 16) */
+typedef struct {
+  int32_t chunk_len, context_len;
+  const int32_t* block_table;
+  int32_t n_blocks;
+} hb_request;
+
+enum { HB_OUT_F32 = 0, HB_OUT_BF16 = 1 };
+
+/* A hybrid batch: requests in any order; token rows of x_in / x_out are the
+ * requests' new tokens concatenated in this order (chunk_len rows each).
+ *   x_in   device bf16 [T][H] layer input (residual stream)
+ *   x_out  device [T][H] layer output, fp32 (HB_OUT_F32) or bf16 (HB_OUT_BF16);
+ *          must not overlap x_in */
+typedef struct {
+  int32_t n_requests;
+  const hb_request* requests;
+  const void* x_in;
+  void* x_out;
+  int32_t out_dtype;
+} hb_batch_desc;
+
+/* Run the decoder layer over the batch: write the new tokens' keys and values
+ * into the cache, then compute x_out. Enqueues on the layer's stream.
+ * Errors: as hb_validate_batch, plus HB_ERR_HIP / HB_ERR_OOM. n_requests == 0
+ * is a no-op. Two requests may read the same block (shared prefix) but must
+ * not write the same slot. */
+hb_status hb_run_iteration(hb_layer* layer, const hb_batch_desc* desc);
+
+/* Check a batch against a layer configuration and pool size without touching
+ * any device (no HIP call). Errors: HB_ERR_INVALID (null pointer,
+ * chunk_len < 1, context_len < 0, short block table, T > max_batch_tokens,
+ * n_requests > max_requests or < 0, bad out_dtype, overlapping x_in/x_out,
+ * two requests writing one slot), HB_ERR_RANGE (a used block id outside
+ * [0, num_blocks)), HB_ERR_UNSUPPORTED (config outside the limits). */
+hb_status hb_validate_batch(const hb_layer_config* cfg, int32_t num_blocks, const hb_batch_desc* desc);
+
+/* Decode load of one profile row: n_decode decodes with the given contexts
+ * (host int32 [n_decode]) next to one prefill chunk starting at chunk_context. */
+typedef struct {
+  int32_t n_decode;
+  const int32_t* decode_contexts;
+  int32_t chunk_context;
+} hb_decode_mix;
+
+/* One profile cell: iteration latency (ms, median / 10th / 90th percentile),
+ * new tokens per second at the median, and the algorithmic HBM bytes and MFMA
+ * flops of the iteration divided by latency and by the MI355X peaks
+ * (8 TB/s, 2.5 PFLOP/s bf16 dense). */
+typedef struct {
+  float median_ms, p10_ms, p90_ms, tokens_per_s, hbm_frac, mfma_frac;
+} hb_profile_cell;
+
+/* Latency profile for dynamic chunking (Section 3.3; the offline profiles of
+ * Section 3.6): for every mix m and chunk size c, synthesise a batch of one
+ * c-token chunk at mix.chunk_context plus the mix's decodes, with block tables
+ * drawn from a seeded permutation of the whole pool, fill the blocks it uses
+ * and its input with seeded pseudo-random bf16, run `warmup` untimed
+ * iterations, then `iters` iterations each preceded by a write of a 512 MiB
+ * buffer (so no data stays in the 256 MB Infinity Cache) and timed with HIP
+ * events. out[m * n_chunk + c] receives the cell. Synchronous. Overwrites the
+ * pool blocks it uses (an offline step). Errors: HB_ERR_INVALID (null
+ * pointer, a batch that does not fit the pool or the layer's capacity,
+ * iters < 1), HB_ERR_OOM, HB_ERR_HIP. */
+hb_status hb_profile(hb_layer* layer, const int32_t* chunk_sizes, int32_t n_chunk,
+                     const hb_decode_mix* mixes, int32_t n_mix, int32_t warmup, int32_t iters,
+                     uint64_t seed, hb_profile_cell* out);
+
+/* Per-kernel timing of hb_run_iteration, for roofline accounting. While
+ * enabled, every launch of an iteration is bracketed by HIP events on the
+ * layer's stream. hb_kernel_times synchronises the stream and adds the elapsed
+ * time (ms) and launch count of each kernel since the last reset into
+ * total_ms[HB_K_COUNT] / launches[HB_K_COUNT]; reset != 0 starts a new tally. */
+enum {
+  HB_K_RMSNORM_ATTN = 0, HB_K_GEMM_QKV, HB_K_ROPE_KV, HB_K_ATTENTION, HB_K_ATTN_MERGE,
+  HB_K_GEMM_O, HB_K_RMSNORM_FFN, HB_K_GEMM_GATE_UP, HB_K_GEMM_DOWN, HB_K_COUNT
+};
+hb_status hb_set_kernel_timing(hb_layer* layer, int32_t enable);
+hb_status hb_kernel_times(hb_layer* layer, double* total_ms, int64_t* launches, int32_t reset);
+const char* hb_kernel_name(int32_t kernel);
+
+/* Intermediate results of the most recent iteration, for per-step checks.
+ * Returns the library-owned device buffer of one step and its row stride in
+ * elements; valid until the next hb_run_iteration or hb_destroy_layer.
+ *   HB_STAGE_Q     bf16 [T][n_q head_dim]  queries after RoPE
+ *   HB_STAGE_ATTN  bf16 [T][n_q head_dim]  attention output (before W_o)
+ *   HB_STAGE_H2    fp32 [T][H]             x + attention @ W_o^T
+ *   HB_STAGE_MLP   bf16 [T][F]             silu(gate) * up */
+enum { HB_STAGE_Q = 0, HB_STAGE_ATTN = 1, HB_STAGE_H2 = 2, HB_STAGE_MLP = 3 };
+hb_status hb_layer_stage(hb_layer* layer, int32_t stage, void** dev_ptr, int64_t* row_stride);
+
+/* Message for the last non-OK status returned on this host thread. */
+const char* hb_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HB_H_ */

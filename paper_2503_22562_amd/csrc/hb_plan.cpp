@@ -1,0 +1,235 @@
+// Host-side validation and planning of a hybrid-batch iteration (no HIP).
+#include "hb_plan.h"
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+namespace hb {
+
+static thread_local std::string g_err;
+
+hb_status fail(hb_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+const char* last_error() { return g_err.c_str(); }
+
+hb_status check_config(const hb_layer_config* c, Dims* d) {
+  if (!c) return fail(HB_ERR_INVALID, "null layer config");
+  if (c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 ||
+      c->ffn_dim <= 0 || c->max_batch_tokens <= 0 || c->max_requests <= 0)
+    return fail(HB_ERR_INVALID, "layer config sizes must be positive");
+  if (!(c->rope_theta > 1.f) || !(c->rms_eps >= 0.f))
+    return fail(HB_ERR_INVALID, "rope_theta must exceed 1 and rms_eps be >= 0");
+  if (c->kv_block_size != 16) return fail(HB_ERR_UNSUPPORTED, "kv_block_size must be 16 (got %d)", c->kv_block_size);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(HB_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", c->head_dim);
+  if (c->n_q_heads % c->n_kv_heads)
+    return fail(HB_ERR_UNSUPPORTED, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)", c->n_q_heads, c->n_kv_heads);
+  int G = c->n_q_heads / c->n_kv_heads;
+  if (G > 16 || 16 % G)
+    return fail(HB_ERR_UNSUPPORTED, "q heads per kv head (%d) must divide 16", G);
+  if (c->hidden % 64) return fail(HB_ERR_UNSUPPORTED, "hidden must be a multiple of 64 (got %d)", c->hidden);
+  if (c->ffn_dim % 16) return fail(HB_ERR_UNSUPPORTED, "ffn_dim must be a multiple of 16 (got %d)", c->ffn_dim);
+  if (c->max_batch_tokens > (1 << 20) || c->max_requests > (1 << 20))
+    return fail(HB_ERR_UNSUPPORTED, "max_batch_tokens / max_requests above 2^20");
+  d->H = c->hidden;
+  d->nq = c->n_q_heads;
+  d->nkv = c->n_kv_heads;
+  d->hd = c->head_dim;
+  d->F = c->ffn_dim;
+  d->blk = 16;
+  d->G = G;
+  d->P = 16 / G;
+  d->qkv_n = (d->nq + 2 * d->nkv) * d->hd;
+  d->theta = c->rope_theta;
+  d->eps = c->rms_eps;
+  d->max_T = c->max_batch_tokens;
+  d->max_R = c->max_requests;
+  return HB_OK;
+}
+
+static int64_t blocks_for(int64_t kv_len) { return (kv_len + 15) / 16; }
+
+hb_status check_batch(const Dims& d, int num_blocks, const hb_batch_desc* desc, SlotMarks* marks) {
+  if (!desc) return fail(HB_ERR_INVALID, "null batch descriptor");
+  const int R = desc->n_requests;
+  if (R < 0) return fail(HB_ERR_INVALID, "n_requests < 0");
+  if (R == 0) return HB_OK;
+  if (R > d.max_R) return fail(HB_ERR_INVALID, "n_requests %d exceeds max_requests %d", R, d.max_R);
+  if (!desc->requests) return fail(HB_ERR_INVALID, "null request array");
+  if (!desc->x_in || !desc->x_out) return fail(HB_ERR_INVALID, "null x_in or x_out");
+  if (desc->out_dtype != HB_OUT_F32 && desc->out_dtype != HB_OUT_BF16)
+    return fail(HB_ERR_INVALID, "out_dtype must be HB_OUT_F32 or HB_OUT_BF16");
+  if (num_blocks <= 0) return fail(HB_ERR_INVALID, "pool has no blocks");
+  int64_t T = 0;
+  for (int r = 0; r < R; ++r) {
+    const hb_request& q = desc->requests[r];
+    if (q.chunk_len < 1) return fail(HB_ERR_INVALID, "request %d: chunk_len %d < 1", r, q.chunk_len);
+    if (q.context_len < 0) return fail(HB_ERR_INVALID, "request %d: context_len %d < 0", r, q.context_len);
+    int64_t kv = (int64_t)q.context_len + q.chunk_len;
+    if (kv > (int64_t)1 << 30) return fail(HB_ERR_INVALID, "request %d: context too long", r);
+    if (!q.block_table) return fail(HB_ERR_INVALID, "request %d: null block_table", r);
+    if (q.n_blocks < blocks_for(kv))
+      return fail(HB_ERR_INVALID, "request %d: block table has %d blocks, needs %lld", r, q.n_blocks,
+                  (long long)blocks_for(kv));
+    for (int64_t i = 0; i < blocks_for(kv); ++i) {
+      int32_t b = q.block_table[i];
+      if (b < 0 || b >= num_blocks)
+        return fail(HB_ERR_RANGE, "request %d: block_table[%lld] = %d outside [0, %d)", r, (long long)i, b, num_blocks);
+    }
+    T += q.chunk_len;
+  }
+  if (T > d.max_T) return fail(HB_ERR_INVALID, "batch has %lld tokens, max_batch_tokens is %d", (long long)T, d.max_T);
+  // x_in (bf16) and x_out must not overlap
+  {
+    uintptr_t a0 = (uintptr_t)desc->x_in, a1 = a0 + (uintptr_t)T * d.H * 2;
+    uintptr_t b0 = (uintptr_t)desc->x_out, b1 = b0 + (uintptr_t)T * d.H * (desc->out_dtype == HB_OUT_F32 ? 4 : 2);
+    if (a0 < b1 && b0 < a1) return fail(HB_ERR_INVALID, "x_out overlaps x_in");
+  }
+  // no two new tokens may be written to the same physical slot
+  SlotMarks local;
+  SlotMarks* m = marks ? marks : &local;
+  if ((int)m->mask.size() < num_blocks) m->mask.assign(num_blocks, 0);
+  m->touched.clear();
+  hb_status st = HB_OK;
+  for (int r = 0; r < R && st == HB_OK; ++r) {
+    const hb_request& q = desc->requests[r];
+    for (int64_t p = q.context_len; p < (int64_t)q.context_len + q.chunk_len; ++p) {
+      int32_t b = q.block_table[p / 16];
+      uint16_t bit = (uint16_t)(1u << (p % 16));
+      if (m->mask[b] == 0) m->touched.push_back(b);
+      if (m->mask[b] & bit) {
+        st = fail(HB_ERR_INVALID, "request %d writes slot %lld of block %d, already written by this batch", r,
+                  (long long)(p % 16), b);
+        break;
+      }
+      m->mask[b] |= bit;
+    }
+  }
+  for (int32_t b : m->touched) m->mask[b] = 0;
+  m->touched.clear();
+  return st;
+}
+
+static int align16(int x) { return (x + 15) & ~15; }
+
+void iteration_work(const Dims& d, const hb_request* reqs, int n, double* flops, double* bytes) {
+  double T = 0, pairs = 0, kv_tokens = 0;
+  for (int r = 0; r < n; ++r) {
+    double c = reqs[r].chunk_len, x = reqs[r].context_len;
+    T += c;
+    pairs += c * x + c * (c + 1) / 2;
+    kv_tokens += x + c;
+  }
+  double p_lin = (double)d.H * d.qkv_n + (double)d.nq * d.hd * d.H + 3.0 * d.H * d.F;
+  *flops = 2.0 * T * p_lin + 4.0 * d.nq * d.hd * pairs;
+  double kv_tok_bytes = 2.0 * d.nkv * d.hd * 2.0;  // K and V, bf16
+  *bytes = 2.0 * p_lin + 2.0 * 2.0 * d.H         // weights and gains, bf16, once
+           + kv_tokens * kv_tok_bytes            // cached + new K/V read once per (request, kv head)
+           + T * kv_tok_bytes                    // new K/V written
+           + T * d.H * 2.0 + T * d.H * 4.0;      // x_in bf16, y fp32
+}
+
+void build_plan(const Dims& d, const hb_batch_desc* desc, int target_items, Plan* p) {
+  const int R = desc->n_requests;
+  const hb_request* rq = desc->requests;
+  int T = 0, nbt = 0;
+  std::vector<int> tok_start(R + 1, 0);
+  for (int r = 0; r < R; ++r) {
+    tok_start[r] = T;
+    T += rq[r].chunk_len;
+    nbt += (int)blocks_for((int64_t)rq[r].context_len + rq[r].chunk_len);
+  }
+  tok_start[R] = T;
+  p->T = T;
+  p->R = R;
+
+  // split length: spread the key work over about target_items waves
+  double total_keys = 0;
+  for (int r = 0; r < R; ++r) {
+    const int c = rq[r].chunk_len, x = rq[r].context_len;
+    for (int i0 = 0; i0 < c; i0 += d.P) total_keys += (double)d.nkv * (x + std::min(c, i0 + d.P));
+  }
+  int S = (int)std::min<double>(1 << 30, total_keys / std::max(1, target_items));
+  S = std::max(256, (S + 31) & ~31);
+  p->split_len = S;
+
+  std::vector<AttnItem> items;
+  std::vector<MergeGroup> groups;
+  int parts = 0;
+  for (int r = 0; r < R; ++r) {
+    const int c = rq[r].chunk_len, x = rq[r].context_len;
+    const int ntiles = (c + d.P - 1) / d.P;
+    for (int g = 0; g < d.nkv; ++g) {
+      // splits of the longest tile define the split count of each tile
+      const int kv_max = x + c;
+      const int nsplit_max = (kv_max + S - 1) / S;
+      std::vector<int> part0(ntiles, -1), nspl(ntiles, 1);
+      for (int t = 0; t < ntiles; ++t) {
+        const int i0 = t * d.P, npos = std::min(d.P, c - i0);
+        const int kv_len = x + i0 + npos;
+        nspl[t] = (kv_len + S - 1) / S;
+        if (nspl[t] > 1) {
+          part0[t] = parts;
+          groups.push_back({parts, nspl[t], tok_start[r] + i0, npos, g, 0, 0, 0});
+          parts += nspl[t];
+        }
+      }
+      for (int s = 0; s < nsplit_max; ++s) {
+        for (int t = 0; t < ntiles; ++t) {
+          if (s >= nspl[t]) continue;
+          const int i0 = t * d.P, npos = std::min(d.P, c - i0);
+          const int kv_len = x + i0 + npos;
+          AttnItem it;
+          it.req = r;
+          it.kv_head = g;
+          it.tok0 = tok_start[r] + i0;
+          it.pos0 = x + i0;
+          it.npos = npos;
+          it.kv_begin = s * S;
+          it.kv_end = std::min(kv_len, (s + 1) * S);
+          it.part = nspl[t] > 1 ? part0[t] + s : -1;
+          items.push_back(it);
+        }
+      }
+    }
+  }
+  p->n_items = (int)items.size();
+  p->n_groups = (int)groups.size();
+  p->n_parts = parts;
+
+  int off = 0;
+  p->off_tok_pos = off;  off += align16(T);
+  p->off_tok_req = off;  off += align16(T);
+  p->off_req_bt = off;   off += align16(R);
+  p->off_bt = off;       off += align16(nbt);
+  p->off_items = off;    off += align16(8 * p->n_items);
+  p->off_groups = off;   off += align16(8 * p->n_groups);
+  p->meta.assign(off, 0);
+  int32_t* m = p->meta.data();
+  int bt_off = 0;
+  for (int r = 0; r < R; ++r) {
+    for (int i = 0; i < rq[r].chunk_len; ++i) {
+      m[p->off_tok_pos + tok_start[r] + i] = rq[r].context_len + i;
+      m[p->off_tok_req + tok_start[r] + i] = r;
+    }
+    m[p->off_req_bt + r] = bt_off;
+    const int nb = (int)blocks_for((int64_t)rq[r].context_len + rq[r].chunk_len);
+    std::memcpy(m + p->off_bt + bt_off, rq[r].block_table, sizeof(int32_t) * nb);
+    bt_off += nb;
+  }
+  if (!items.empty()) std::memcpy(m + p->off_items, items.data(), sizeof(AttnItem) * items.size());
+  if (!groups.empty()) std::memcpy(m + p->off_groups, groups.data(), sizeof(MergeGroup) * groups.size());
+  iteration_work(d, rq, R, &p->flops, &p->bytes);
+}
+
+}  // namespace hb

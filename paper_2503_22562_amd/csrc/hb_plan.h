@@ -1,0 +1,71 @@
+// Host-side planning of one hybrid-batch iteration (no HIP calls).
+//
+// Turns a batch descriptor into the int32 metadata the kernels read: per-token
+// position and request, per-request block-table offset, the block ids, the
+// attention work list and the split-merge groups. Everything is packed into
+// one array so one host-to-device copy moves it.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "hb.h"
+
+namespace hb {
+
+// Set the thread-local message returned by hb_last_error(); returns `st`.
+hb_status fail(hb_status st, const char* fmt, ...);
+const char* last_error();
+
+struct Dims {
+  int H = 0, nq = 0, nkv = 0, hd = 0, F = 0, blk = 16;
+  int G = 0;      // q heads per kv head
+  int P = 0;      // query positions per 16-column attention tile = 16 / G
+  int qkv_n = 0;  // (nq + 2 nkv) * hd
+  float theta = 0.f, eps = 0.f;
+  int max_T = 0, max_R = 0;
+};
+
+hb_status check_config(const hb_layer_config* cfg, Dims* d);
+
+// One wave of attention work: 16 query columns (P positions x G heads of one
+// kv head) of one request over the key positions [kv_begin, kv_end).
+struct AttnItem {
+  int32_t req, kv_head, tok0, pos0, npos, kv_begin, kv_end, part;  // part < 0: final
+};
+// A tile whose key range was split over `nparts` consecutive partial slots.
+struct MergeGroup {
+  int32_t part0, nparts, tok0, npos, kv_head, pad0, pad1, pad2;
+};
+static_assert(sizeof(AttnItem) == 32 && sizeof(MergeGroup) == 32, "packed as 8 int32");
+
+struct Plan {
+  int T = 0, R = 0;
+  int n_items = 0, n_groups = 0, n_parts = 0;
+  int split_len = 0;
+  // offsets (int32 units) of each section inside meta
+  int off_tok_pos = 0, off_tok_req = 0, off_req_bt = 0, off_bt = 0, off_items = 0, off_groups = 0;
+  std::vector<int32_t> meta;
+  // algorithmic work of the iteration (for roofline accounting)
+  double flops = 0, bytes = 0;
+};
+
+// Scratch reused across calls for the duplicate-slot check.
+struct SlotMarks {
+  std::vector<uint16_t> mask;    // per block: bit o set when slot o is written
+  std::vector<int32_t> touched;  // blocks to clear afterwards
+};
+
+// Validate `desc` against the layer shape and a pool of num_blocks blocks.
+hb_status check_batch(const Dims& d, int num_blocks, const hb_batch_desc* desc, SlotMarks* marks);
+
+// Build the plan of a validated batch. `target_items` steers the split of
+// long key ranges (about the number of waves that fill the GPU).
+void build_plan(const Dims& d, const hb_batch_desc* desc, int target_items, Plan* p);
+
+// Algorithmic flops and HBM bytes of one iteration (what the method must
+// compute and move, not what an implementation happens to do).
+void iteration_work(const Dims& d, const hb_request* reqs, int n, double* flops, double* bytes);
+
+}  // namespace hb

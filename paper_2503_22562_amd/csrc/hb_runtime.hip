@@ -1,0 +1,536 @@
+// Host runtime behind the C ABI: layer object, workspace, metadata staging,
+// the launch sequence of one iteration, per-kernel timing and the latency
+// profiler.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include <hip/hip_runtime.h>
+
+#include "hb.h"
+#include "hb_kernels.h"
+#include "hb_plan.h"
+
+using namespace hb;
+
+#define HB_HIP(call)                                                                        \
+  do {                                                                                      \
+    hipError_t e_ = (call);                                                                 \
+    if (e_ != hipSuccess) return fail(HB_ERR_HIP, "%s failed: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+namespace {
+constexpr int kStages = 4;
+constexpr double kPeakHbm = 8.0e12;      // MI355X HBM3E, bytes/s
+constexpr double kPeakBf16 = 2.5e15;     // MI355X dense bf16 MFMA, flop/s
+
+struct Stage {
+  int32_t* host = nullptr;  // pinned
+  size_t cap = 0;           // int32 elements
+  hipEvent_t done = nullptr;
+  bool pending = false;
+};
+
+struct TimedLaunch {
+  hipEvent_t start, stop;
+  int kernel;
+};
+}  // namespace
+
+struct hb_layer {
+  Dims d;
+  hb_layer_weights w{};
+  hb_kv_pool pool{};
+  hipStream_t stream = nullptr;
+  int device = 0, cu_count = 0;
+  // workspace
+  uint16_t *xn = nullptr, *qkv = nullptr, *q_rot = nullptr, *attn = nullptr, *mlp = nullptr;
+  float* h2 = nullptr;
+  double* inv_freq = nullptr;
+  float *part_o = nullptr, *part_ml = nullptr;
+  int part_cap = 0;
+  int32_t* meta = nullptr;
+  size_t meta_cap = 0;
+  Stage stage[kStages];
+  int stage_next = 0;
+  SlotMarks marks;
+  Plan plan;
+  int last_T = 0;
+  // timing
+  bool timing = false;
+  std::vector<hipEvent_t> ev_free;
+  std::vector<TimedLaunch> timed;
+  double tot_ms[HB_K_COUNT] = {};
+  int64_t launches[HB_K_COUNT] = {};
+};
+
+namespace {
+
+hb_status ensure_meta(hb_layer* L, size_t n) {
+  if (n <= L->meta_cap) return HB_OK;
+  size_t cap = std::max(n, L->meta_cap * 2);
+  HB_HIP(hipStreamSynchronize(L->stream));
+  if (L->meta) HB_HIP(hipFree(L->meta));
+  L->meta = nullptr;
+  L->meta_cap = 0;
+  if (hipMalloc(&L->meta, cap * sizeof(int32_t)) != hipSuccess) return fail(HB_ERR_OOM, "metadata buffer of %zu B", cap * 4);
+  L->meta_cap = cap;
+  return HB_OK;
+}
+
+hb_status ensure_parts(hb_layer* L, int n) {
+  if (n <= L->part_cap) return HB_OK;
+  int cap = std::max(n, L->part_cap * 2);
+  HB_HIP(hipStreamSynchronize(L->stream));
+  if (L->part_o) HB_HIP(hipFree(L->part_o));
+  if (L->part_ml) HB_HIP(hipFree(L->part_ml));
+  L->part_o = L->part_ml = nullptr;
+  L->part_cap = 0;
+  if (hipMalloc(&L->part_o, (size_t)cap * 16 * L->d.hd * sizeof(float)) != hipSuccess ||
+      hipMalloc(&L->part_ml, (size_t)cap * 16 * 2 * sizeof(float)) != hipSuccess)
+    return fail(HB_ERR_OOM, "attention split buffers for %d parts", cap);
+  L->part_cap = cap;
+  return HB_OK;
+}
+
+// Copy `n` int32 from host to L->meta through the pinned staging ring.
+hb_status stage_upload(hb_layer* L, const int32_t* src, size_t n, int32_t* dst) {
+  Stage& s = L->stage[L->stage_next];
+  L->stage_next = (L->stage_next + 1) % kStages;
+  if (s.pending) {
+    HB_HIP(hipEventSynchronize(s.done));
+    s.pending = false;
+  }
+  if (n > s.cap) {
+    if (s.host) HB_HIP(hipHostFree(s.host));
+    s.host = nullptr;
+    s.cap = 0;
+    size_t cap = std::max<size_t>(n, 1 << 16);
+    if (hipHostMalloc((void**)&s.host, cap * sizeof(int32_t), hipHostMallocDefault) != hipSuccess)
+      return fail(HB_ERR_OOM, "pinned staging of %zu B", cap * 4);
+    s.cap = cap;
+  }
+  std::memcpy(s.host, src, n * sizeof(int32_t));
+  HB_HIP(hipMemcpyAsync(dst, s.host, n * sizeof(int32_t), hipMemcpyHostToDevice, L->stream));
+  HB_HIP(hipEventRecord(s.done, L->stream));
+  s.pending = true;
+  return HB_OK;
+}
+
+hb_status collect_timing(hb_layer* L) {
+  if (L->timed.empty()) return HB_OK;
+  HB_HIP(hipStreamSynchronize(L->stream));
+  for (const TimedLaunch& t : L->timed) {
+    float ms = 0.f;
+    HB_HIP(hipEventElapsedTime(&ms, t.start, t.stop));
+    L->tot_ms[t.kernel] += ms;
+    L->launches[t.kernel] += 1;
+    L->ev_free.push_back(t.start);
+    L->ev_free.push_back(t.stop);
+  }
+  L->timed.clear();
+  return HB_OK;
+}
+
+hb_status get_event(hb_layer* L, hipEvent_t* e) {
+  if (L->ev_free.empty()) {
+    HB_HIP(hipEventCreate(e));
+    return HB_OK;
+  }
+  *e = L->ev_free.back();
+  L->ev_free.pop_back();
+  return HB_OK;
+}
+
+// Launch wrapper: brackets the launch with events while timing is enabled.
+template <typename F>
+hb_status timed(hb_layer* L, int kernel, F&& launch) {
+  if (!L->timing) {
+    launch();
+    return HB_OK;
+  }
+  if (L->timed.size() >= 4096) {
+    hb_status st = collect_timing(L);
+    if (st != HB_OK) return st;
+  }
+  TimedLaunch t;
+  t.kernel = kernel;
+  hb_status st = get_event(L, &t.start);
+  if (st == HB_OK) st = get_event(L, &t.stop);
+  if (st != HB_OK) return st;
+  HB_HIP(hipEventRecord(t.start, L->stream));
+  launch();
+  HB_HIP(hipEventRecord(t.stop, L->stream));
+  L->timed.push_back(t);
+  return HB_OK;
+}
+
+void free_layer(hb_layer* L) {
+  if (!L) return;
+  (void)hipStreamSynchronize(L->stream);
+  for (void* p : {(void*)L->xn, (void*)L->qkv, (void*)L->q_rot, (void*)L->attn, (void*)L->mlp, (void*)L->h2,
+                  (void*)L->inv_freq, (void*)L->part_o, (void*)L->part_ml, (void*)L->meta})
+    if (p) (void)hipFree(p);
+  for (Stage& s : L->stage) {
+    if (s.host) (void)hipHostFree(s.host);
+    if (s.done) (void)hipEventDestroy(s.done);
+  }
+  for (const TimedLaunch& t : L->timed) {
+    (void)hipEventDestroy(t.start);
+    (void)hipEventDestroy(t.stop);
+  }
+  for (hipEvent_t e : L->ev_free) (void)hipEventDestroy(e);
+  delete L;
+}
+
+hb_status check_hip(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(HB_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return HB_OK;
+}
+
+// Enqueue the whole layer for a planned batch.
+hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
+  const Dims& d = L->d;
+  Plan& p = L->plan;
+  const int T = p.T;
+  hb_status st = ensure_meta(L, p.meta.size());
+  if (st == HB_OK) st = ensure_parts(L, p.n_parts);
+  if (st != HB_OK) return st;
+  st = stage_upload(L, p.meta.data(), p.meta.size(), L->meta);
+  if (st != HB_OK) return st;
+  hipStream_t s = L->stream;
+  const int32_t* meta = L->meta;
+  const uint16_t* x_in = static_cast<const uint16_t*>(desc->x_in);
+
+  st = timed(L, HB_K_RMSNORM_ATTN, [&] {
+    launch_rmsnorm(s, x_in, false, static_cast<const uint16_t*>(L->w.g_attn), L->xn, T, d.H, d.eps);
+  });
+  if (st != HB_OK) return st;
+
+  GemmArgs g{};
+  g.A = L->xn; g.lda = d.H;
+  g.B = static_cast<const uint16_t*>(L->w.w_qkv); g.ldb = d.H;
+  g.M = T; g.N = d.qkv_n; g.K = d.H;
+  g.C = L->qkv; g.ldc = d.qkv_n; g.epi = GEMM_STORE_BF16;
+  st = timed(L, HB_K_GEMM_QKV, [&] { launch_gemm(s, g); });
+  if (st != HB_OK) return st;
+
+  RopeKvArgs r{};
+  r.qkv = L->qkv; r.T = T; r.nq = d.nq; r.nkv = d.nkv; r.hd = d.hd;
+  r.tok_pos = meta + p.off_tok_pos; r.tok_req = meta + p.off_tok_req;
+  r.req_bt = meta + p.off_req_bt; r.bt = meta + p.off_bt;
+  r.inv_freq = L->inv_freq; r.q_out = L->q_rot;
+  r.k_pool = static_cast<uint16_t*>(L->pool.k_pool); r.v_pool = static_cast<uint16_t*>(L->pool.v_pool);
+  st = timed(L, HB_K_ROPE_KV, [&] { launch_rope_kv(s, r); });
+  if (st != HB_OK) return st;
+
+  AttnArgs at{};
+  at.q = L->q_rot; at.o = L->attn;
+  at.k_pool = r.k_pool; at.v_pool = r.v_pool;
+  at.items = meta + p.off_items; at.n_items = p.n_items;
+  at.groups = meta + p.off_groups; at.n_groups = p.n_groups;
+  at.req_bt = r.req_bt; at.bt = r.bt;
+  at.part_o = L->part_o; at.part_ml = L->part_ml;
+  at.nq = d.nq; at.nkv = d.nkv; at.hd = d.hd;
+  at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.hd));
+  st = timed(L, HB_K_ATTENTION, [&] { launch_attention(s, at); });
+  if (st != HB_OK) return st;
+  if (p.n_groups > 0) {
+    st = timed(L, HB_K_ATTN_MERGE, [&] { launch_attn_merge(s, at); });
+    if (st != HB_OK) return st;
+  }
+
+  g = GemmArgs{};
+  g.A = L->attn; g.lda = d.nq * d.hd;
+  g.B = static_cast<const uint16_t*>(L->w.w_o); g.ldb = d.nq * d.hd;
+  g.M = T; g.N = d.H; g.K = d.nq * d.hd;
+  g.C = L->h2; g.ldc = d.H; g.c_f32 = 1;
+  g.R = x_in; g.ldr = d.H; g.r_f32 = 0; g.epi = GEMM_RESIDUAL;
+  st = timed(L, HB_K_GEMM_O, [&] { launch_gemm(s, g); });
+  if (st != HB_OK) return st;
+
+  st = timed(L, HB_K_RMSNORM_FFN, [&] {
+    launch_rmsnorm(s, L->h2, true, static_cast<const uint16_t*>(L->w.g_ffn), L->xn, T, d.H, d.eps);
+  });
+  if (st != HB_OK) return st;
+
+  g = GemmArgs{};
+  g.A = L->xn; g.lda = d.H;
+  g.B = static_cast<const uint16_t*>(L->w.w_gate_up); g.ldb = d.H;
+  g.M = T; g.N = d.F; g.K = d.H;
+  g.C = L->mlp; g.ldc = d.F; g.epi = GEMM_SWIGLU;
+  st = timed(L, HB_K_GEMM_GATE_UP, [&] { launch_gemm(s, g); });
+  if (st != HB_OK) return st;
+
+  g = GemmArgs{};
+  g.A = L->mlp; g.lda = d.F;
+  g.B = static_cast<const uint16_t*>(L->w.w_down); g.ldb = d.F;
+  g.M = T; g.N = d.H; g.K = d.F;
+  g.C = desc->x_out; g.ldc = d.H; g.c_f32 = desc->out_dtype == HB_OUT_F32;
+  g.R = L->h2; g.ldr = d.H; g.r_f32 = 1; g.epi = GEMM_RESIDUAL;
+  st = timed(L, HB_K_GEMM_DOWN, [&] { launch_gemm(s, g); });
+  if (st != HB_OK) return st;
+  L->last_T = T;
+  return check_hip("kernel launch");
+}
+
+int target_items(const hb_layer* L) { return std::max(256, L->cu_count * 16); }
+
+// splitmix64 stream for the profiler's host-side draws
+struct SplitMix {
+  uint64_t s;
+  uint64_t next() {
+    uint64_t z = (s += 0x9E3779B97F4A7C15ull);
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+  }
+};
+
+}  // namespace
+
+extern "C" {
+
+const char* hb_last_error(void) { return last_error(); }
+
+hb_status hb_validate_batch(const hb_layer_config* cfg, int32_t num_blocks, const hb_batch_desc* desc) {
+  Dims d;
+  hb_status st = check_config(cfg, &d);
+  if (st != HB_OK) return st;
+  return check_batch(d, num_blocks, desc, nullptr);
+}
+
+hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w, const hb_kv_pool* pool,
+                          void* hip_stream, hb_layer** out) {
+  if (!out) return fail(HB_ERR_INVALID, "null output handle");
+  *out = nullptr;
+  Dims d;
+  hb_status st = check_config(cfg, &d);
+  if (st != HB_OK) return st;
+  if (d.H > 16384) return fail(HB_ERR_UNSUPPORTED, "hidden above 16384");
+  if (!w || !w->w_qkv || !w->w_o || !w->w_gate_up || !w->w_down || !w->g_attn || !w->g_ffn)
+    return fail(HB_ERR_INVALID, "null weight pointer");
+  if (!pool || !pool->k_pool || !pool->v_pool || pool->num_blocks <= 0)
+    return fail(HB_ERR_INVALID, "null or empty KV pool");
+  hb_layer* L = new (std::nothrow) hb_layer();
+  if (!L) return fail(HB_ERR_OOM, "host allocation of the layer");
+  L->d = d;
+  L->w = *w;
+  L->pool = *pool;
+  L->stream = static_cast<hipStream_t>(hip_stream);
+  auto bail = [&](hb_status s) { free_layer(L); return s; };
+  if (hipGetDevice(&L->device) != hipSuccess) return bail(fail(HB_ERR_HIP, "hipGetDevice failed"));
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, L->device) != hipSuccess) return bail(fail(HB_ERR_HIP, "hipGetDeviceProperties failed"));
+  L->cu_count = prop.multiProcessorCount;
+  const size_t T = d.max_T;
+  struct Alloc { void** p; size_t bytes; } allocs[] = {
+      {(void**)&L->xn, T * d.H * 2},         {(void**)&L->qkv, T * d.qkv_n * 2},
+      {(void**)&L->q_rot, T * d.nq * d.hd * 2}, {(void**)&L->attn, T * d.nq * d.hd * 2},
+      {(void**)&L->mlp, T * d.F * 2},        {(void**)&L->h2, T * d.H * 4},
+      {(void**)&L->inv_freq, (size_t)d.hd / 2 * sizeof(double)},
+  };
+  for (auto& a : allocs)
+    if (hipMalloc(a.p, a.bytes) != hipSuccess) return bail(fail(HB_ERR_OOM, "workspace allocation of %zu B", a.bytes));
+  std::vector<double> inv(d.hd / 2);
+  for (int j = 0; j < d.hd / 2; ++j) inv[j] = std::pow((double)d.theta, -2.0 * j / d.hd);
+  if (hipMemcpy(L->inv_freq, inv.data(), inv.size() * sizeof(double), hipMemcpyHostToDevice) != hipSuccess)
+    return bail(fail(HB_ERR_HIP, "upload of RoPE frequencies failed"));
+  for (Stage& s : L->stage)
+    if (hipEventCreateWithFlags(&s.done, hipEventDisableTiming) != hipSuccess)
+      return bail(fail(HB_ERR_HIP, "hipEventCreate failed"));
+  st = ensure_meta(L, (size_t)1 << 18);
+  if (st == HB_OK) st = ensure_parts(L, 1024);
+  if (st != HB_OK) return bail(st);
+  *out = L;
+  return HB_OK;
+}
+
+void hb_destroy_layer(hb_layer* layer) { free_layer(layer); }
+
+hb_status hb_append_kv(hb_layer* L, const int32_t* block_table, int32_t n_blocks, int32_t context_len,
+                       int32_t n_tokens, const void* k, const void* v) {
+  if (!L) return fail(HB_ERR_INVALID, "null layer");
+  if (n_tokens < 0 || context_len < 0) return fail(HB_ERR_INVALID, "negative n_tokens or context_len");
+  if (n_tokens == 0) return HB_OK;
+  if (!block_table || !k || !v) return fail(HB_ERR_INVALID, "null block_table, k or v");
+  const int64_t kv = (int64_t)context_len + n_tokens;
+  if (kv > ((int64_t)1 << 30)) return fail(HB_ERR_INVALID, "context too long");
+  const int64_t nb = (kv + 15) / 16;
+  if (n_blocks < nb) return fail(HB_ERR_INVALID, "block table has %d blocks, needs %lld", n_blocks, (long long)nb);
+  for (int64_t i = context_len / 16; i < nb; ++i)
+    if (block_table[i] < 0 || block_table[i] >= L->pool.num_blocks)
+      return fail(HB_ERR_RANGE, "block_table[%lld] = %d outside [0, %d)", (long long)i, block_table[i],
+                  L->pool.num_blocks);
+  hb_status st = ensure_meta(L, (size_t)nb);
+  if (st != HB_OK) return st;
+  st = stage_upload(L, block_table, (size_t)nb, L->meta);
+  if (st != HB_OK) return st;
+  launch_append_kv(L->stream, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), n_tokens,
+                   context_len, L->meta, L->d.nkv, L->d.hd, static_cast<uint16_t*>(L->pool.k_pool),
+                   static_cast<uint16_t*>(L->pool.v_pool));
+  return check_hip("append_kv launch");
+}
+
+hb_status hb_run_iteration(hb_layer* L, const hb_batch_desc* desc) {
+  if (!L) return fail(HB_ERR_INVALID, "null layer");
+  hb_status st = check_batch(L->d, L->pool.num_blocks, desc, &L->marks);
+  if (st != HB_OK) return st;
+  if (desc->n_requests == 0) return HB_OK;
+  build_plan(L->d, desc, target_items(L), &L->plan);
+  return enqueue_layer(L, desc);
+}
+
+hb_status hb_set_kernel_timing(hb_layer* L, int32_t enable) {
+  if (!L) return fail(HB_ERR_INVALID, "null layer");
+  L->timing = enable != 0;
+  return HB_OK;
+}
+
+hb_status hb_kernel_times(hb_layer* L, double* total_ms, int64_t* launches, int32_t reset) {
+  if (!L) return fail(HB_ERR_INVALID, "null layer");
+  hb_status st = collect_timing(L);
+  if (st != HB_OK) return st;
+  for (int k = 0; k < HB_K_COUNT; ++k) {
+    if (total_ms) total_ms[k] = L->tot_ms[k];
+    if (launches) launches[k] = L->launches[k];
+  }
+  if (reset) {
+    std::fill(L->tot_ms, L->tot_ms + HB_K_COUNT, 0.0);
+    std::fill(L->launches, L->launches + HB_K_COUNT, (int64_t)0);
+  }
+  return HB_OK;
+}
+
+const char* hb_kernel_name(int32_t k) {
+  static const char* names[HB_K_COUNT] = {"rmsnorm_attn", "gemm_qkv",  "rope_kv",        "attention", "attn_merge",
+                                          "gemm_o",       "rmsnorm_ffn", "gemm_gate_up", "gemm_down"};
+  return (k >= 0 && k < HB_K_COUNT) ? names[k] : "unknown";
+}
+
+hb_status hb_layer_stage(hb_layer* L, int32_t stage, void** dev_ptr, int64_t* row_stride) {
+  if (!L || !dev_ptr || !row_stride) return fail(HB_ERR_INVALID, "null argument");
+  switch (stage) {
+    case HB_STAGE_Q: *dev_ptr = L->q_rot; *row_stride = (int64_t)L->d.nq * L->d.hd; break;
+    case HB_STAGE_ATTN: *dev_ptr = L->attn; *row_stride = (int64_t)L->d.nq * L->d.hd; break;
+    case HB_STAGE_H2: *dev_ptr = L->h2; *row_stride = L->d.H; break;
+    case HB_STAGE_MLP: *dev_ptr = L->mlp; *row_stride = L->d.F; break;
+    default: return fail(HB_ERR_INVALID, "unknown stage %d", stage);
+  }
+  return HB_OK;
+}
+
+hb_status hb_profile(hb_layer* L, const int32_t* chunk_sizes, int32_t n_chunk, const hb_decode_mix* mixes,
+                     int32_t n_mix, int32_t warmup, int32_t iters, uint64_t seed, hb_profile_cell* out) {
+  if (!L || !chunk_sizes || !mixes || !out) return fail(HB_ERR_INVALID, "null argument");
+  if (n_chunk < 1 || n_mix < 1 || iters < 1 || warmup < 0) return fail(HB_ERR_INVALID, "empty grid or iters < 1");
+  const Dims& d = L->d;
+  const int NB = L->pool.num_blocks;
+  // validate every cell before touching the device
+  for (int mi = 0; mi < n_mix; ++mi) {
+    const hb_decode_mix& mx = mixes[mi];
+    if (mx.n_decode < 0 || (mx.n_decode > 0 && !mx.decode_contexts) || mx.chunk_context < 0)
+      return fail(HB_ERR_INVALID, "mix %d malformed", mi);
+    int64_t dec_blocks = 0;
+    for (int i = 0; i < mx.n_decode; ++i) {
+      if (mx.decode_contexts[i] < 0) return fail(HB_ERR_INVALID, "mix %d: negative decode context", mi);
+      dec_blocks += (mx.decode_contexts[i] + 1 + 15) / 16;
+    }
+    for (int ci = 0; ci < n_chunk; ++ci) {
+      const int c = chunk_sizes[ci];
+      if (c < 1) return fail(HB_ERR_INVALID, "chunk size %d < 1", c);
+      if ((int64_t)c + mx.n_decode > d.max_T || 1 + mx.n_decode > d.max_R)
+        return fail(HB_ERR_INVALID, "cell (%d, mix %d) exceeds the layer's batch capacity", c, mi);
+      if (dec_blocks + ((int64_t)mx.chunk_context + c + 15) / 16 > NB)
+        return fail(HB_ERR_INVALID, "cell (%d, mix %d) needs more blocks than the pool holds", c, mi);
+    }
+  }
+  int max_c = 0;
+  for (int ci = 0; ci < n_chunk; ++ci) max_c = std::max(max_c, chunk_sizes[ci]);
+  int max_dec = 0;
+  for (int mi = 0; mi < n_mix; ++mi) max_dec = std::max(max_dec, mixes[mi].n_decode);
+  const int64_t maxT = (int64_t)max_c + max_dec;
+  const int64_t flush_bytes = (int64_t)512 << 20;
+  void *x_in = nullptr, *x_out = nullptr, *flush = nullptr;
+  int32_t* blocks_dev = nullptr;
+  std::vector<hipEvent_t> ev;
+  hb_status st = HB_OK;
+  auto cleanup = [&]() {
+    (void)hipStreamSynchronize(L->stream);
+    if (x_in) (void)hipFree(x_in);
+    if (x_out) (void)hipFree(x_out);
+    if (flush) (void)hipFree(flush);
+    if (blocks_dev) (void)hipFree(blocks_dev);
+    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+  };
+  if (hipMalloc(&x_in, maxT * d.H * 2) != hipSuccess || hipMalloc(&x_out, maxT * d.H * 4) != hipSuccess ||
+      hipMalloc(&flush, flush_bytes) != hipSuccess || hipMalloc(&blocks_dev, (size_t)NB * sizeof(int32_t)) != hipSuccess) {
+    cleanup();
+    return fail(HB_ERR_OOM, "profiler buffers");
+  }
+  ev.resize(2 * (size_t)iters);
+  for (auto& e : ev)
+    if (hipEventCreate(&e) != hipSuccess) { cleanup(); return fail(HB_ERR_HIP, "hipEventCreate failed"); }
+  launch_fill_random_bf16(L->stream, static_cast<uint16_t*>(x_in), maxT * d.H, seed ^ 0xA5A5u, 1.7f);
+
+  std::vector<int32_t> perm(NB);
+  std::vector<hb_request> reqs;
+  std::vector<float> lat(iters);
+  for (int mi = 0; mi < n_mix && st == HB_OK; ++mi) {
+    const hb_decode_mix& mx = mixes[mi];
+    for (int ci = 0; ci < n_chunk && st == HB_OK; ++ci) {
+      const int c = chunk_sizes[ci];
+      // block ids: seeded Fisher-Yates permutation of the pool, consumed in request order
+      SplitMix rng{seed * 1000003ull + (uint64_t)mi * 7919ull + (uint64_t)ci};
+      for (int i = 0; i < NB; ++i) perm[i] = i;
+      for (int i = NB - 1; i > 0; --i) std::swap(perm[i], perm[rng.next() % (uint64_t)(i + 1)]);
+      reqs.clear();
+      int used = 0;
+      reqs.push_back({c, mx.chunk_context, perm.data() + used, (mx.chunk_context + c + 15) / 16});
+      used += reqs.back().n_blocks;
+      for (int i = 0; i < mx.n_decode; ++i) {
+        reqs.push_back({1, mx.decode_contexts[i], perm.data() + used, (mx.decode_contexts[i] + 1 + 15) / 16});
+        used += reqs.back().n_blocks;
+      }
+      if (hipMemcpyAsync(blocks_dev, perm.data(), (size_t)used * 4, hipMemcpyHostToDevice, L->stream) != hipSuccess ||
+          hipStreamSynchronize(L->stream) != hipSuccess) {
+        st = fail(HB_ERR_HIP, "profiler block upload failed");
+        break;
+      }
+      launch_fill_blocks(L->stream, blocks_dev, used, d.nkv, d.hd, static_cast<uint16_t*>(L->pool.k_pool),
+                         static_cast<uint16_t*>(L->pool.v_pool), seed + (uint64_t)used);
+      hb_batch_desc desc{(int32_t)reqs.size(), reqs.data(), x_in, x_out, HB_OUT_F32};
+      for (int i = 0; i < warmup && st == HB_OK; ++i) st = hb_run_iteration(L, &desc);
+      for (int i = 0; i < iters && st == HB_OK; ++i) {
+        launch_flush(L->stream, flush, flush_bytes, (uint32_t)i);
+        if (hipEventRecord(ev[2 * i], L->stream) != hipSuccess) st = fail(HB_ERR_HIP, "hipEventRecord failed");
+        if (st == HB_OK) st = hb_run_iteration(L, &desc);
+        if (st == HB_OK && hipEventRecord(ev[2 * i + 1], L->stream) != hipSuccess)
+          st = fail(HB_ERR_HIP, "hipEventRecord failed");
+      }
+      if (st != HB_OK) break;
+      if (hipStreamSynchronize(L->stream) != hipSuccess) { st = fail(HB_ERR_HIP, "profiler sync failed"); break; }
+      for (int i = 0; i < iters; ++i) hipEventElapsedTime(&lat[i], ev[2 * i], ev[2 * i + 1]);
+      std::vector<float> sorted = lat;
+      std::sort(sorted.begin(), sorted.end());
+      auto pct = [&](double q) { return sorted[std::min<size_t>(sorted.size() - 1, (size_t)(q * (sorted.size() - 1) + 0.5))]; };
+      hb_profile_cell& cell = out[mi * n_chunk + ci];
+      cell.median_ms = pct(0.5);
+      cell.p10_ms = pct(0.1);
+      cell.p90_ms = pct(0.9);
+      double flops, bytes;
+      iteration_work(d, reqs.data(), (int)reqs.size(), &flops, &bytes);
+      const double sec = cell.median_ms * 1e-3;
+      cell.tokens_per_s = (float)((c + mx.n_decode) / sec);
+      cell.hbm_frac = (float)(bytes / sec / kPeakHbm);
+      cell.mfma_frac = (float)(flops / sec / kPeakBf16);
+    }
+  }
+  cleanup();
+  return st;
+}
+
+}  // extern "C"

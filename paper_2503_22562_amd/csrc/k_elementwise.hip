@@ -1,0 +1,199 @@
+// Bandwidth-bound kernels of the layer: RMSNorm, RoPE + paged KV scatter,
+// the KV append copy, and the profiling fills.
+#include "hb_device.h"
+#include "hb_kernels.h"
+
+namespace hb {
+
+// ---------------------------------------------------------------------------
+// RMSNorm: one 256-thread workgroup per token row; each thread holds up to
+// MAXV vectors of 8 elements in registers between the reduction and the scale.
+// ---------------------------------------------------------------------------
+template <bool F32IN, int MAXV>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const void* __restrict__ x, const uint16_t* __restrict__ g,
+                                                      uint16_t* __restrict__ out, int H, float eps) {
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const int nvec = H >> 3;
+  float v[MAXV][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int vi = tid + 256 * i;
+    if (vi < nvec) {
+      if (F32IN) {
+        const float* xr = reinterpret_cast<const float*>(x) + (size_t)row * H + 8 * vi;
+        u32x4 a = ld16(xr), b = ld16(xr + 4);
+        for (int j = 0; j < 4; ++j) { v[i][j] = __uint_as_float(a[j]); v[i][4 + j] = __uint_as_float(b[j]); }
+      } else {
+        const uint16_t* xr = reinterpret_cast<const uint16_t*>(x) + (size_t)row * H + 8 * vi;
+        u32x4 a = ld16(xr);
+        for (int j = 0; j < 4; ++j) { v[i][2 * j] = bf16_lo(a[j]); v[i][2 * j + 1] = bf16_hi(a[j]); }
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ss += v[i][j] * v[i][j];
+    }
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float r = 1.0f / sqrtf(tot / (float)H + eps);
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int vi = tid + 256 * i;
+    if (vi < nvec) {
+      u32x4 gw = ld16(g + 8 * vi), o;
+      for (int j = 0; j < 4; ++j)
+        o[j] = pack_bf16x2(v[i][2 * j] * r * bf16_lo(gw[j]), v[i][2 * j + 1] * r * bf16_hi(gw[j]));
+      st16(out + (size_t)row * H + 8 * vi, o);
+    }
+  }
+}
+
+void launch_rmsnorm(hipStream_t s, const void* x, bool x_f32, const uint16_t* g, uint16_t* out, int T, int H,
+                    float eps) {
+  if (T <= 0) return;
+  const int nvec = H / 8;
+  if (nvec <= 256) {
+    if (x_f32) rmsnorm_kernel<true, 1><<<T, 256, 0, s>>>(x, g, out, H, eps);
+    else rmsnorm_kernel<false, 1><<<T, 256, 0, s>>>(x, g, out, H, eps);
+  } else if (nvec <= 1024) {
+    if (x_f32) rmsnorm_kernel<true, 4><<<T, 256, 0, s>>>(x, g, out, H, eps);
+    else rmsnorm_kernel<false, 4><<<T, 256, 0, s>>>(x, g, out, H, eps);
+  } else {
+    if (x_f32) rmsnorm_kernel<true, 8><<<T, 256, 0, s>>>(x, g, out, H, eps);
+    else rmsnorm_kernel<false, 8><<<T, 256, 0, s>>>(x, g, out, H, eps);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// RoPE + KV scatter: one workgroup per token. Angles p * theta^(-2j/hd) are
+// formed and evaluated in fp64, then rounded to fp32 for the rotation.
+// K goes to k_pool[blk][g][slot][d], V to v_pool[blk][g][d][slot].
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
+  __shared__ float cs[64], sn[64];
+  const int t = blockIdx.x, tid = threadIdx.x;
+  const int hd = a.hd, half = hd >> 1;
+  const int p = a.tok_pos[t];
+  if (tid < half) {
+    double sv, cv;
+    sincos((double)p * a.inv_freq[tid], &sv, &cv);
+    cs[tid] = (float)cv;
+    sn[tid] = (float)sv;
+  }
+  __syncthreads();
+  const uint16_t* row = a.qkv + (size_t)t * (a.nq + 2 * a.nkv) * hd;
+  // queries
+  for (int idx = tid; idx < a.nq * half; idx += 256) {
+    const int h = idx / half, j = idx - h * half;
+    const float u = bf16_to_f32(row[h * hd + j]), w = bf16_to_f32(row[h * hd + j + half]);
+    uint16_t* qo = a.q_out + (size_t)t * a.nq * hd + h * hd;
+    qo[j] = (uint16_t)f32_to_bf16(u * cs[j] - w * sn[j]);
+    qo[j + half] = (uint16_t)f32_to_bf16(w * cs[j] + u * sn[j]);
+  }
+  const int blk = a.bt[a.req_bt[a.tok_req[t]] + (p >> 4)];
+  const int slot = p & 15;
+  // keys (rotated) -> k_pool
+  const uint16_t* krow = row + a.nq * hd;
+  for (int idx = tid; idx < a.nkv * half; idx += 256) {
+    const int g = idx / half, j = idx - g * half;
+    const float u = bf16_to_f32(krow[g * hd + j]), w = bf16_to_f32(krow[g * hd + j + half]);
+    uint16_t* ko = a.k_pool + (((size_t)blk * a.nkv + g) * 16 + slot) * hd;
+    ko[j] = (uint16_t)f32_to_bf16(u * cs[j] - w * sn[j]);
+    ko[j + half] = (uint16_t)f32_to_bf16(w * cs[j] + u * sn[j]);
+  }
+  // values -> v_pool (dim-major inside the block)
+  const uint16_t* vrow = krow + a.nkv * hd;
+  for (int idx = tid; idx < a.nkv * hd; idx += 256) {
+    const int g = idx / hd, d = idx - g * hd;
+    a.v_pool[(((size_t)blk * a.nkv + g) * hd + d) * 16 + slot] = vrow[idx];
+  }
+}
+
+void launch_rope_kv(hipStream_t s, const RopeKvArgs& a) {
+  if (a.T <= 0) return;
+  rope_kv_kernel<<<a.T, 256, 0, s>>>(a);
+}
+
+// ---------------------------------------------------------------------------
+// KV append: one workgroup per token, a pure copy into the token's slot.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void append_kv_kernel(const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+                                                        int ctx, const int32_t* __restrict__ bt, int nkv, int hd,
+                                                        uint16_t* __restrict__ k_pool, uint16_t* __restrict__ v_pool) {
+  const int t = blockIdx.x;
+  const int p = ctx + t;
+  const int blk = bt[p >> 4], slot = p & 15;
+  const int n = nkv * hd;
+  for (int idx = threadIdx.x; idx < n; idx += 256) {
+    const int g = idx / hd, d = idx - g * hd;
+    k_pool[(((size_t)blk * nkv + g) * 16 + slot) * hd + d] = k[(size_t)t * n + idx];
+    v_pool[(((size_t)blk * nkv + g) * hd + d) * 16 + slot] = v[(size_t)t * n + idx];
+  }
+}
+
+void launch_append_kv(hipStream_t s, const uint16_t* k, const uint16_t* v, int n_tokens, int ctx, const int32_t* bt,
+                      int nkv, int hd, uint16_t* k_pool, uint16_t* v_pool) {
+  if (n_tokens <= 0) return;
+  append_kv_kernel<<<n_tokens, 256, 0, s>>>(k, v, ctx, bt, nkv, hd, k_pool, v_pool);
+}
+
+// ---------------------------------------------------------------------------
+// Profiling fills: counter-based hash (splitmix64 finaliser) -> uniform in
+// [-scale, scale) -> bf16.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+__device__ __forceinline__ uint16_t rand_bf16(uint64_t seed, uint64_t i, float scale) {
+  const uint64_t h = mix64(seed * 0x9E3779B97F4A7C15ull + i);
+  const float u = (float)(h >> 40) * (1.0f / 16777216.0f);  // [0,1)
+  return (uint16_t)f32_to_bf16((2.f * u - 1.f) * scale);
+}
+
+__global__ void fill_random_kernel(uint16_t* p, int64_t n, uint64_t seed, float scale) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = rand_bf16(seed, (uint64_t)i, scale);
+}
+
+void launch_fill_random_bf16(hipStream_t s, uint16_t* p, int64_t n, uint64_t seed, float scale) {
+  if (n <= 0) return;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  fill_random_kernel<<<(int)blocks, 256, 0, s>>>(p, n, seed, scale);
+}
+
+__global__ void fill_blocks_kernel(const int32_t* blocks, int nkv, int hd, uint16_t* k_pool, uint16_t* v_pool,
+                                   uint64_t seed) {
+  const int64_t per = (int64_t)nkv * 16 * hd;
+  const int64_t b = blocks[blockIdx.x];
+  for (int64_t i = threadIdx.x; i < per; i += blockDim.x) {
+    k_pool[b * per + i] = rand_bf16(seed, (uint64_t)(b * per + i) * 2, 1.7f);
+    v_pool[b * per + i] = rand_bf16(seed, (uint64_t)(b * per + i) * 2 + 1, 1.7f);
+  }
+}
+
+void launch_fill_blocks(hipStream_t s, const int32_t* blocks, int n, int nkv, int hd, uint16_t* k_pool,
+                        uint16_t* v_pool, uint64_t seed) {
+  if (n <= 0) return;
+  fill_blocks_kernel<<<n, 256, 0, s>>>(blocks, nkv, hd, k_pool, v_pool, seed);
+}
+
+__global__ void flush_kernel(u32x4* p, int64_t n, uint32_t value) {
+  const u32x4 v = {value, value, value, value};
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+void launch_flush(hipStream_t s, void* buf, int64_t bytes, uint32_t value) {
+  const int64_t n = bytes / 16;
+  if (n <= 0) return;
+  flush_kernel<<<4096, 256, 0, s>>>(reinterpret_cast<u32x4*>(buf), n, value);
+}
+
+}  // namespace hb

@@ -1,0 +1,240 @@
+"""Python binding of libhb.so (include/hb.h): argument marshalling only.
+
+Every step of the layer runs in the library's HIP kernels; PyTorch supplies
+device memory and streams. Names and arguments follow the C ABI.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Dict, Iterable, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhb.so")
+
+HB_OK, HB_ERR_INVALID, HB_ERR_RANGE, HB_ERR_OOM, HB_ERR_HIP, HB_ERR_UNSUPPORTED = range(6)
+HB_OUT_F32, HB_OUT_BF16 = 0, 1
+(HB_K_RMSNORM_ATTN, HB_K_GEMM_QKV, HB_K_ROPE_KV, HB_K_ATTENTION, HB_K_ATTN_MERGE, HB_K_GEMM_O,
+ HB_K_RMSNORM_FFN, HB_K_GEMM_GATE_UP, HB_K_GEMM_DOWN, HB_K_COUNT) = range(10)
+HB_STAGE_Q, HB_STAGE_ATTN, HB_STAGE_H2, HB_STAGE_MLP = range(4)
+
+EXPORTED = ("hb_create_layer", "hb_destroy_layer", "hb_append_kv", "hb_run_iteration", "hb_validate_batch",
+            "hb_profile", "hb_set_kernel_timing", "hb_kernel_times", "hb_kernel_name", "hb_layer_stage",
+            "hb_last_error")
+
+
+class hb_layer_config(C.Structure):
+    _fields_ = [("hidden", C.c_int32), ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("ffn_dim", C.c_int32), ("kv_block_size", C.c_int32),
+                ("rope_theta", C.c_float), ("rms_eps", C.c_float),
+                ("max_batch_tokens", C.c_int32), ("max_requests", C.c_int32)]
+
+
+class hb_layer_weights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("w_qkv", "w_o", "w_gate_up", "w_down", "g_attn", "g_ffn")]
+
+
+class hb_kv_pool(C.Structure):
+    _fields_ = [("k_pool", C.c_void_p), ("v_pool", C.c_void_p), ("num_blocks", C.c_int32)]
+
+
+class hb_request(C.Structure):
+    _fields_ = [("chunk_len", C.c_int32), ("context_len", C.c_int32),
+                ("block_table", C.POINTER(C.c_int32)), ("n_blocks", C.c_int32)]
+
+
+class hb_batch_desc(C.Structure):
+    _fields_ = [("n_requests", C.c_int32), ("requests", C.POINTER(hb_request)),
+                ("x_in", C.c_void_p), ("x_out", C.c_void_p), ("out_dtype", C.c_int32)]
+
+
+class hb_decode_mix(C.Structure):
+    _fields_ = [("n_decode", C.c_int32), ("decode_contexts", C.POINTER(C.c_int32)), ("chunk_context", C.c_int32)]
+
+
+class hb_profile_cell(C.Structure):
+    _fields_ = [(n, C.c_float) for n in ("median_ms", "p10_ms", "p90_ms", "tokens_per_s", "hbm_frac", "mfma_frac")]
+
+
+class HBError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"hb status {status}: {message}")
+        self.status = status
+
+
+_lib: Optional[C.CDLL] = None
+
+
+def load() -> C.CDLL:
+    """Load libhb.so; raises if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2503_22562_amd.build`")
+    # torch first: libhb then binds to the HIP runtime torch already loaded,
+    # so torch's streams and allocations are valid handles for the library.
+    import torch  # noqa: F401
+    lib = C.CDLL(LIB_PATH)
+    st = C.c_int
+    lib.hb_create_layer.argtypes = [C.POINTER(hb_layer_config), C.POINTER(hb_layer_weights), C.POINTER(hb_kv_pool),
+                                    C.c_void_p, C.POINTER(C.c_void_p)]
+    lib.hb_create_layer.restype = st
+    lib.hb_destroy_layer.argtypes = [C.c_void_p]
+    lib.hb_destroy_layer.restype = None
+    lib.hb_append_kv.argtypes = [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
+                                 C.c_void_p]
+    lib.hb_append_kv.restype = st
+    lib.hb_run_iteration.argtypes = [C.c_void_p, C.POINTER(hb_batch_desc)]
+    lib.hb_run_iteration.restype = st
+    lib.hb_validate_batch.argtypes = [C.POINTER(hb_layer_config), C.c_int32, C.POINTER(hb_batch_desc)]
+    lib.hb_validate_batch.restype = st
+    lib.hb_profile.argtypes = [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.POINTER(hb_decode_mix), C.c_int32,
+                               C.c_int32, C.c_int32, C.c_uint64, C.POINTER(hb_profile_cell)]
+    lib.hb_profile.restype = st
+    lib.hb_set_kernel_timing.argtypes = [C.c_void_p, C.c_int32]
+    lib.hb_set_kernel_timing.restype = st
+    lib.hb_kernel_times.argtypes = [C.c_void_p, C.POINTER(C.c_double), C.POINTER(C.c_int64), C.c_int32]
+    lib.hb_kernel_times.restype = st
+    lib.hb_kernel_name.argtypes = [C.c_int32]
+    lib.hb_kernel_name.restype = C.c_char_p
+    lib.hb_layer_stage.argtypes = [C.c_void_p, C.c_int32, C.POINTER(C.c_void_p), C.POINTER(C.c_int64)]
+    lib.hb_layer_stage.restype = st
+    lib.hb_last_error.argtypes = []
+    lib.hb_last_error.restype = C.c_char_p
+    _lib = lib
+    return lib
+
+
+def hb_last_error() -> str:
+    return load().hb_last_error().decode()
+
+
+def _check(status: int) -> None:
+    if status != HB_OK:
+        raise HBError(status, hb_last_error())
+
+
+def make_config(shape, max_batch_tokens: int, max_requests: int) -> hb_layer_config:
+    """hb_layer_config from any object with the layer-shape attributes."""
+    return hb_layer_config(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn_dim,
+                           getattr(shape, "kv_block", 16), float(shape.rope_theta), float(shape.rms_eps),
+                           int(max_batch_tokens), int(max_requests))
+
+
+class Layer:
+    """Owns an hb_layer handle and keeps the tensors it points at alive."""
+
+    def __init__(self, handle: C.c_void_p, cfg: hb_layer_config, keep: list):
+        self.handle = handle
+        self.cfg = cfg
+        self._keep = keep
+
+    def __del__(self):
+        try:
+            hb_destroy_layer(self)
+        except Exception:
+            pass
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def hb_create_layer(cfg: hb_layer_config, weights: Dict[str, "torch.Tensor"], k_pool, v_pool,
+                    num_blocks: int, stream: Optional[int] = None) -> Layer:
+    lib = load()
+    w = hb_layer_weights(*(_ptr(weights[n]) for n in ("w_qkv", "w_o", "w_gate_up", "w_down", "g_attn", "g_ffn")))
+    pool = hb_kv_pool(_ptr(k_pool), _ptr(v_pool), int(num_blocks))
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream().cuda_stream
+    h = C.c_void_p()
+    _check(lib.hb_create_layer(C.byref(cfg), C.byref(w), C.byref(pool), C.c_void_p(stream), C.byref(h)))
+    return Layer(h, cfg, [weights, k_pool, v_pool])
+
+
+def hb_destroy_layer(layer: Layer) -> None:
+    if layer.handle is not None and layer.handle.value:
+        load().hb_destroy_layer(layer.handle)
+        layer.handle = None
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def hb_append_kv(layer: Layer, block_table, context_len: int, k, v) -> None:
+    bt = _i32(block_table)
+    n = 0 if k is None else int(k.shape[0])
+    _check(load().hb_append_kv(layer.handle, bt.ctypes.data_as(C.POINTER(C.c_int32)), len(bt), int(context_len), n,
+                               C.c_void_p(_ptr(k)), C.c_void_p(_ptr(v))))
+
+
+def _desc(requests: Sequence[Tuple[int, int, Iterable[int]]], x_in_ptr: int, x_out_ptr: int, out_dtype: int):
+    tables = [_i32(bt) for (_, _, bt) in requests]
+    arr = (hb_request * max(1, len(requests)))()
+    for i, ((c, x, _), bt) in enumerate(zip(requests, tables)):
+        arr[i] = hb_request(int(c), int(x), bt.ctypes.data_as(C.POINTER(C.c_int32)), len(bt))
+    d = hb_batch_desc(len(requests), arr, C.c_void_p(x_in_ptr), C.c_void_p(x_out_ptr), int(out_dtype))
+    return d, (tables, arr)
+
+
+def hb_run_iteration(layer: Layer, requests: Sequence[Tuple[int, int, Iterable[int]]], x_in, x_out,
+                     out_dtype: Optional[int] = None) -> None:
+    """requests: (chunk_len, context_len, block_table) per request, in row order."""
+    if out_dtype is None:
+        import torch
+        out_dtype = HB_OUT_F32 if x_out.dtype == torch.float32 else HB_OUT_BF16
+    d, keep = _desc(requests, _ptr(x_in), _ptr(x_out), out_dtype)
+    _check(load().hb_run_iteration(layer.handle, C.byref(d)))
+
+
+def hb_validate_batch(cfg: hb_layer_config, num_blocks: int, requests, x_in_ptr: int, x_out_ptr: int,
+                      out_dtype: int = HB_OUT_F32) -> int:
+    """Host-only check; returns the status code (no exception)."""
+    d, keep = _desc(requests, x_in_ptr, x_out_ptr, out_dtype)
+    return load().hb_validate_batch(C.byref(cfg), int(num_blocks), C.byref(d))
+
+
+def hb_profile(layer: Layer, chunk_sizes: Sequence[int], mixes: Sequence[Tuple[Sequence[int], int]],
+               warmup: int = 10, iters: int = 100, seed: int = 0) -> np.ndarray:
+    """mixes: (decode_contexts, chunk_context) per row. Returns a structured array [n_mix][n_chunk]."""
+    cs = _i32(chunk_sizes)
+    ctxs = [_i32(m[0]) for m in mixes]
+    marr = (hb_decode_mix * len(mixes))()
+    for i, (c, (_, cc)) in enumerate(zip(ctxs, mixes)):
+        marr[i] = hb_decode_mix(len(c), c.ctypes.data_as(C.POINTER(C.c_int32)), int(cc))
+    out = (hb_profile_cell * (len(mixes) * len(cs)))()
+    _check(load().hb_profile(layer.handle, cs.ctypes.data_as(C.POINTER(C.c_int32)), len(cs), marr, len(mixes),
+                             int(warmup), int(iters), C.c_uint64(seed), out))
+    names = [f[0] for f in hb_profile_cell._fields_]
+    res = np.zeros((len(mixes), len(cs)), dtype=[(n, np.float64) for n in names])
+    for i in range(len(mixes)):
+        for j in range(len(cs)):
+            cell = out[i * len(cs) + j]
+            res[i, j] = tuple(getattr(cell, n) for n in names)
+    return res
+
+
+def hb_set_kernel_timing(layer: Layer, enable: bool) -> None:
+    _check(load().hb_set_kernel_timing(layer.handle, 1 if enable else 0))
+
+
+def hb_kernel_times(layer: Layer, reset: bool = False) -> Dict[str, Tuple[float, int]]:
+    ms = (C.c_double * HB_K_COUNT)()
+    n = (C.c_int64 * HB_K_COUNT)()
+    _check(load().hb_kernel_times(layer.handle, ms, n, 1 if reset else 0))
+    return {hb_kernel_name(k): (ms[k], n[k]) for k in range(HB_K_COUNT)}
+
+
+def hb_kernel_name(k: int) -> str:
+    return load().hb_kernel_name(int(k)).decode()
+
+
+def hb_layer_stage(layer: Layer, stage: int) -> Tuple[int, int]:
+    p = C.c_void_p()
+    s = C.c_int64()
+    _check(load().hb_layer_stage(layer.handle, int(stage), C.byref(p), C.byref(s)))
+    return int(p.value or 0), int(s.value)

@@ -1,0 +1,118 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every entry point include/hb.h declares, and rejects malformed batches with
+the documented status before any device work (hb_validate_batch makes no HIP
+call)."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def H():
+    from paper_2503_22562_amd import hb
+    try:
+        hb.load()
+    except RuntimeError as e:
+        pytest.fail(str(e))
+    return hb
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "hb.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hb_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("hb_create_layer", "hb_append_kv", "hb_run_iteration", "hb_profile", "hb_destroy_layer",
+              "hb_validate_batch", "hb_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(H):
+    lib = H.load()
+    for n in declared_functions():
+        assert hasattr(lib, n), f"libhb.so does not export {n}"
+    assert set(declared_functions()) == set(H.EXPORTED)
+
+
+def test_kernel_names(H):
+    names = [H.hb_kernel_name(k) for k in range(H.HB_K_COUNT)]
+    assert len(set(names)) == H.HB_K_COUNT and "attention" in names
+    assert H.hb_kernel_name(99) == "unknown"
+
+
+class Shape:
+    hidden, n_q_heads, n_kv_heads, head_dim, ffn_dim = 256, 4, 2, 64, 688
+    rope_theta, rms_eps, kv_block = 5e5, 1e-5, 16
+
+
+X_IN, X_OUT = 0x10000000, 0x20000000  # fake device addresses: never dereferenced
+
+
+def _v(H, reqs, num_blocks=64, max_T=128, max_R=8, shape=Shape, x_in=X_IN, x_out=X_OUT, out_dtype=0):
+    cfg = H.make_config(shape, max_T, max_R)
+    return H.hb_validate_batch(cfg, num_blocks, reqs, x_in, x_out, out_dtype)
+
+
+def bt(*ids):
+    return np.array(ids, dtype=np.int32)
+
+
+def test_valid_batches(H):
+    assert _v(H, []) == H.HB_OK
+    assert _v(H, [(64, 128, np.arange(12)), (1, 256, np.arange(20, 37))]) == H.HB_OK
+    # shared read-only prefix blocks, distinct written slots
+    assert _v(H, [(1, 16, bt(3, 4)), (1, 16, bt(3, 5))]) == H.HB_OK
+    # two requests writing different slots of one block
+    assert _v(H, [(1, 3, bt(7)), (1, 4, bt(7))]) == H.HB_OK
+
+
+@pytest.mark.parametrize("reqs,status", [
+    ([(0, 0, bt(1))], "INVALID"),                       # chunk_len < 1
+    ([(1, -1, bt(1))], "INVALID"),                      # context_len < 0
+    ([(17, 0, bt(1))], "INVALID"),                      # block table too short
+    ([(1, 16, bt(1))], "INVALID"),                      # position 16 needs a second block
+    ([(1, 0, bt(64))], "RANGE"),                        # block id == num_blocks
+    ([(1, 0, bt(-1))], "RANGE"),                        # negative block id
+    ([(1, 5, bt(2)), (1, 5, bt(2))], "INVALID"),        # two tokens, one slot
+    ([(4, 0, bt(2)), (1, 3, bt(2))], "INVALID"),        # chunk overlaps a decode's slot
+    ([(129, 0, np.arange(9))], "INVALID"),              # T above max_batch_tokens
+    ([(1, 0, bt(i)) for i in range(9)], "INVALID"),     # above max_requests
+])
+def test_invalid_batches(H, reqs, status):
+    assert _v(H, reqs) == getattr(H, "HB_ERR_" + status)
+    assert H.hb_last_error()
+
+
+def test_pointer_and_dtype_errors(H):
+    r = [(2, 0, bt(1))]
+    assert _v(H, r, x_in=0) == H.HB_ERR_INVALID
+    assert _v(H, r, x_out=0) == H.HB_ERR_INVALID
+    assert _v(H, r, out_dtype=7) == H.HB_ERR_INVALID
+    # x_out overlapping x_in
+    assert _v(H, r, x_out=X_IN + 256) == H.HB_ERR_INVALID
+    assert _v(H, r, x_out=X_IN + 2 * 256 * 2) == H.HB_OK
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 96, "UNSUPPORTED"),
+    ("kv_block", 32, "UNSUPPORTED"),
+    ("n_kv_heads", 3, "UNSUPPORTED"),
+    ("hidden", 200, "UNSUPPORTED"),
+    ("ffn_dim", 100, "UNSUPPORTED"),
+    ("hidden", 0, "INVALID"),
+])
+def test_config_errors(H, field, value, status):
+    shape = type("S", (Shape,), {field: value})
+    assert _v(H, [(1, 0, bt(1))], shape=shape) == getattr(H, "HB_ERR_" + status)
+
+
+def test_gqa_group_must_divide_16(H):
+    shape = type("S", (Shape,), {"n_q_heads": 32, "n_kv_heads": 1})
+    assert _v(H, [(1, 0, bt(1))], shape=shape) == H.HB_ERR_UNSUPPORTED

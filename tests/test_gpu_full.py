@@ -1,0 +1,88 @@
+"""GPU parity at the full Llama-3 8B / 70B layer shapes, in the launch
+configuration the benchmark times, against the fp64 oracle on sampled rows
+(each chunk's first and last rows, random middle rows, random decodes); plus
+the latency-profile property dynamic chunking relies on."""
+import numpy as np
+import pytest
+
+import oracle
+from hb_workloads import (LLAMA3_8B, LLAMA3_70B, SWEEP_CHUNKS, SWEEP_DECODES, llama70b_batch, llama8b_batch,
+                          make_weights, multi_batch, sweep_batch, sweep_decode_contexts)
+from hbref import assert_parity, errors, oracle_for_batch, sample_rows
+
+pytestmark = pytest.mark.gpu
+
+_CACHE = {}
+
+
+def _device_layer(shape, max_T, max_R):
+    """One device layer per shape for the module (weights + 2M-token pool)."""
+    from paper_2503_22562_amd.harness import DeviceLayer
+    key = shape.name
+    if key not in _CACHE:
+        _CACHE.clear()
+        import torch
+        torch.cuda.empty_cache()
+        w = make_weights(shape)
+        from hb_workloads import POOL_TOKENS
+        dl = DeviceLayer(shape, w, POOL_TOKENS // 16, max_T, max_R)
+        _CACHE[key] = (dl, w, oracle.weights_to_f64(w))
+    return _CACHE[key]
+
+
+def _check_batch(b, max_T=4096, max_R=512, seed=0):
+    import torch
+    from paper_2503_22562_amd.harness import to_device_bf16
+    dl, w, w64 = _device_layer(b.shape, max_T, max_R)
+    for r, req in enumerate(b.requests):
+        if req.context_len:
+            k, v = b.prior_kv(r)
+            dl.append_kv(req.block_table, 0, k, v)
+    x_bits = b.x_in()
+    y = dl.run([(q.chunk_len, q.context_len, q.block_table) for q in b.requests], to_device_bf16(x_bits))
+    torch.cuda.synchronize()
+    y = y.cpu().numpy()
+    assert np.all(np.isfinite(y))
+    rows = sample_rows(b, seed=seed)
+    ref = oracle_for_batch(b, w64, rows=rows, x_bits=x_bits)
+    ma, rl = errors(y[rows], ref)
+    print(f"{b.label}: T={b.n_tokens} rows checked={len(rows)} max-abs={ma:.3e} rel-L2={rl:.3e}")
+    assert_parity(y[rows], ref, b.label)
+
+
+def test_llama8b_chunk512_plus_64_decodes(hb):
+    _check_batch(llama8b_batch())
+
+
+def test_llama8b_four_chunks_plus_256_decodes(hb):
+    _check_batch(multi_batch())
+
+
+@pytest.mark.parametrize("chunk,n_dec", [(2048, 0), (128, 256), (1024, 32)])
+def test_llama8b_sweep_cells(hb, chunk, n_dec):
+    _check_batch(sweep_batch(chunk, n_dec))
+
+
+@pytest.mark.timeout(900)
+def test_llama70b_chunk2048_plus_32_decodes(hb):
+    _check_batch(llama70b_batch(), max_T=2080, max_R=64)
+
+
+def test_latency_profile_monotone_in_chunk_size(hb):
+    """Bigger chunks take longer per iteration and give more tokens/s (the
+    chunk-size trade-off of the dynamic-chunking section). Criterion: for each
+    decode count the median latency does not decrease with chunk size, except
+    for ties within 1% on the weight-streaming plateau (chunks 128 and 256
+    without decodes)."""
+    from paper_2503_22562_amd import hb as H
+    dl, _, _ = _device_layer(LLAMA3_8B, 4096, 512)
+    mixes = [(sweep_decode_contexts(n), 0) for n in SWEEP_DECODES]
+    prof = H.hb_profile(dl.layer, SWEEP_CHUNKS, mixes, warmup=3, iters=15, seed=1)
+    med = prof["median_ms"]
+    print("median ms\n", np.round(med, 4))
+    print("tokens/s\n", np.round(prof["tokens_per_s"]))
+    for i, n in enumerate(SWEEP_DECODES):
+        for j in range(1, len(SWEEP_CHUNKS)):
+            slack = 1.01 if (n == 0 and SWEEP_CHUNKS[j] <= 256) else 1.0
+            assert med[i, j] * slack >= med[i, j - 1], f"n_dec={n}: latency drops from chunk {SWEEP_CHUNKS[j-1]} to {SWEEP_CHUNKS[j]}"
+    assert np.all(prof["tokens_per_s"][:, -1] > prof["tokens_per_s"][:, 0])

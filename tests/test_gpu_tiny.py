@@ -1,0 +1,241 @@
+"""GPU parity of the hybrid-batch layer against the fp64 oracle on small
+shapes, KV placement bit-exactness, invariants and edge cases. Every call
+goes through the C ABI (libhb.so)."""
+import numpy as np
+import pytest
+
+import oracle
+from hb_workloads import (TINY, LayerShape, f32_to_bf16_bits, make_batch, make_weights, tiny_batch)
+from hbref import assert_parity, assert_stage, errors, oracle_for_batch
+
+pytestmark = pytest.mark.gpu
+
+
+def _setup(hb, batch, weights=None, max_T=None, max_R=None, seed_prior=True):
+    from paper_2503_22562_amd.harness import DeviceLayer
+    w = make_weights(batch.shape) if weights is None else weights
+    dl = DeviceLayer(batch.shape, w, batch.num_blocks, max_T or max(batch.n_tokens, 1),
+                     max_R or max(len(batch.requests), 1))
+    if seed_prior:
+        for r, req in enumerate(batch.requests):
+            if req.context_len:
+                k, v = batch.prior_kv(r)
+                dl.append_kv(req.block_table, 0, k, v)
+    return dl, w
+
+
+def _reqs(batch):
+    return [(r.chunk_len, r.context_len, r.block_table) for r in batch.requests]
+
+
+def _run(dl, batch, x_bits=None):
+    import torch
+    from paper_2503_22562_amd.harness import to_device_bf16
+    x = to_device_bf16(batch.x_in() if x_bits is None else x_bits)
+    y = dl.run(_reqs(batch), x)
+    torch.cuda.synchronize()
+    return y.cpu().numpy().astype(np.float64)
+
+
+def test_tiny_parity_all_rows_and_stages(hb):
+    from paper_2503_22562_amd import hb as H
+    from paper_2503_22562_amd.harness import bf16_bits
+    b = tiny_batch()
+    dl, w = _setup(hb, b)
+    y = _run(dl, b)
+    ref, st = oracle_for_batch(b, oracle.weights_to_f64(w), stages=True)
+    print("tiny y", errors(y, ref))
+    assert_parity(y, ref)
+    T = b.n_tokens
+    q = oracle.bf16_bits_to_f64(bf16_bits(dl.stage(H.HB_STAGE_Q, T)))
+    assert_stage(q, st["q"].reshape(T, -1), "q after RoPE")
+    o = oracle.bf16_bits_to_f64(bf16_bits(dl.stage(H.HB_STAGE_ATTN, T)))
+    assert_stage(o, st["o"], "attention output")
+    h2 = dl.stage(H.HB_STAGE_H2, T).cpu().numpy()
+    assert_parity(h2, st["h2"], "h2")
+    m = oracle.bf16_bits_to_f64(bf16_bits(dl.stage(H.HB_STAGE_MLP, T)))
+    assert_stage(m, st["m"], "silu(gate)*up")
+
+
+SMALL_SHAPES = [
+    LayerShape("g8-hd64", 512, 8, 1, 64, 256, weight_seed=11),
+    LayerShape("g1-hd128", 512, 4, 4, 128, 336, weight_seed=12),
+    LayerShape("g16-hd64", 1024, 16, 1, 64, 512, weight_seed=13),
+    LayerShape("g4-hd128", 1024, 8, 2, 128, 688, weight_seed=14),
+]
+
+
+@pytest.mark.parametrize("shape", SMALL_SHAPES, ids=lambda s: s.name)
+def test_small_shapes_parity(hb, shape):
+    lens = [(37, 21), (1, 0), (1, 15), (1, 16), (100, 0), (1, 300), (5, 3)]
+    b = make_batch(shape, lens, seed=77, num_blocks=128)
+    dl, w = _setup(hb, b)
+    y = _run(dl, b)
+    ref = oracle_for_batch(b, oracle.weights_to_f64(w))
+    print(shape.name, errors(y, ref))
+    assert_parity(y, ref)
+
+
+def _expected_slots(batch, which):
+    """{(block, kv_head, slot): bits[hd]} of the prior context (which = 0 K, 1 V)."""
+    out = {}
+    for r, req in enumerate(batch.requests):
+        if not req.context_len:
+            continue
+        kv = batch.prior_kv(r)[which]
+        for p in range(req.context_len):
+            blk, s = oracle.kv_slot(req.block_table, p)
+            for g in range(batch.shape.n_kv_heads):
+                out[(blk, g, s)] = kv[p, g]
+    return out
+
+
+def _pool_bits(dl):
+    from paper_2503_22562_amd.harness import bf16_bits
+    return bf16_bits(dl.k_pool), bf16_bits(dl.v_pool)
+
+
+def test_append_kv_placement_bit_exact(hb):
+    lens = [(3, 45), (1, 16), (1, 1), (20, 31), (1, 0)]
+    b = make_batch(TINY, lens, seed=5, num_blocks=64)
+    dl, _ = _setup(hb, b)
+    kp, vp = _pool_bits(dl)
+    k_exp, v_exp = _expected_slots(b, 0), _expected_slots(b, 1)
+    touched_k = np.zeros(kp.shape[:3], dtype=bool)
+    for (blk, g, s), bits in k_exp.items():
+        np.testing.assert_array_equal(kp[blk, g, s], bits)
+        touched_k[blk, g, s] = True
+    for (blk, g, s), bits in v_exp.items():
+        np.testing.assert_array_equal(vp[blk, g, :, s], bits)
+    assert np.all(kp[~touched_k] == 0xFFFF), "append_kv wrote K outside its slots"
+    assert np.all(vp.transpose(0, 1, 3, 2)[~touched_k] == 0xFFFF), "append_kv wrote V outside its slots"
+
+
+def test_run_writes_exactly_the_new_slots(hb):
+    lens = [(23, 9), (1, 32), (1, 47), (16, 0)]
+    b = make_batch(TINY, lens, seed=6, num_blocks=64)
+    dl, w = _setup(hb, b)
+    k0, v0 = _pool_bits(dl)
+    _run(dl, b)
+    k1, v1 = _pool_bits(dl)
+    new = np.zeros(k0.shape[:3], dtype=bool)
+    for req in b.requests:
+        for p in range(req.context_len, req.kv_len):
+            blk, s = oracle.kv_slot(req.block_table, p)
+            new[blk, :, s] = True
+    changed_k = np.any(k1 != k0, axis=-1)
+    changed_v = np.any(v1 != v0, axis=-2)
+    np.testing.assert_array_equal(changed_k, new)
+    np.testing.assert_array_equal(changed_v, new)
+    # the stored values are the rotated keys and the values of the new tokens
+    _, st = oracle_for_batch(b, oracle.weights_to_f64(w), stages=True)
+    starts = b.token_offsets()
+    for r, req in enumerate(b.requests):
+        for i in range(req.chunk_len):
+            blk, s = oracle.kv_slot(req.block_table, req.context_len + i)
+            t = starts[r] + i
+            assert_stage(oracle.bf16_bits_to_f64(k1[blk, :, s]), st["k"][t], "stored K")
+            assert_stage(oracle.bf16_bits_to_f64(v1[blk, :, :, s]), st["v"][t], "stored V")
+
+
+def test_block_table_permutation_is_bit_exact(hb):
+    lens = [(40, 50), (1, 70), (1, 3)]
+    b1 = make_batch(TINY, lens, seed=8, num_blocks=64)
+    b2 = make_batch(TINY, lens, seed=9, num_blocks=64)  # same data, other block ids
+    b2.seed = b1.seed
+    assert any(not np.array_equal(r1.block_table, r2.block_table) for r1, r2 in zip(b1.requests, b2.requests))
+    w = make_weights(TINY)
+    y1 = _run(_setup(hb, b1, w)[0], b1)
+    y2 = _run(_setup(hb, b2, w)[0], b2)
+    np.testing.assert_array_equal(y1, y2)
+
+
+def test_request_order_permutes_rows_bit_exact(hb):
+    lens = [(12, 30), (1, 40), (7, 0), (1, 18)]
+    b = make_batch(TINY, lens, seed=10, num_blocks=64)
+    dl, w = _setup(hb, b)
+    x = b.x_in()
+    y = _run(dl, b, x)
+    order = [3, 0, 2, 1]
+    starts = b.token_offsets()
+    rows = np.concatenate([np.arange(starts[r], starts[r + 1]) for r in order])
+    bp = make_batch(TINY, [lens[r] for r in order], seed=10, num_blocks=64)
+    for i, r in enumerate(order):
+        bp.requests[i].block_table = b.requests[r].block_table
+    yp = _run(dl, bp, x[rows])
+    np.testing.assert_array_equal(yp, y[rows])
+
+
+def test_chunk_split_matches_unsplit(hb):
+    w = make_weights(TINY)
+    L = 70
+    full = make_batch(TINY, [(L, 0), (1, 20)], seed=12, num_blocks=64)
+    x_prompt = full.x_in()[:L]
+    dl, _ = _setup(hb, full, w)
+    x_full = full.x_in()
+    y_full = _run(dl, full, x_full)[:L]
+    ref = oracle_for_batch(full, oracle.weights_to_f64(w))[:L]
+    assert_parity(y_full, ref, "unsplit")
+    # same prompt, same blocks, as 4 chunks in successive iterations next to a decode
+    dl2, _ = _setup(hb, full, w)
+    bt = full.requests[0].block_table
+    ys = []
+    for s, e in [(0, 7), (7, 30), (30, 31), (31, 70)]:
+        part = make_batch(TINY, [(e - s, s)], seed=12, num_blocks=64)
+        part.requests[0].block_table = bt
+        ys.append(_run(dl2, part, x_prompt[s:e]))
+    y_split = np.concatenate(ys)
+    assert_parity(y_split, ref, "split")
+    assert_parity(y_split, y_full, "split vs unsplit", max_abs=1e-2, rel_l2=5e-3)
+
+
+def test_edge_cases_positions_and_capacity(hb):
+    # decode at position 0, decodes on block boundaries, a chunk that fills
+    # the batch capacity exactly, block tables longer than needed
+    lens = [(1, 0), (1, 15), (1, 16), (1, 31), (45, 17)]
+    b = make_batch(TINY, lens, seed=13, num_blocks=64)
+    b.requests[1].block_table = np.concatenate([b.requests[1].block_table, [63, 62]]).astype(np.int32)
+    dl, w = _setup(hb, b, max_T=b.n_tokens, max_R=len(lens))
+    y = _run(dl, b)
+    ref = oracle_for_batch(b, oracle.weights_to_f64(w))
+    assert_parity(y, ref)
+
+
+def test_empty_batch_is_noop_and_errors_touch_nothing(hb):
+    import torch
+    from paper_2503_22562_amd import hb as H
+    b = make_batch(TINY, [(5, 10), (1, 3)], seed=14, num_blocks=16)
+    dl, _ = _setup(hb, b)
+    k0, v0 = _pool_bits(dl)
+    x = torch.zeros((8, TINY.hidden), dtype=torch.bfloat16, device="cuda")
+    out = torch.full((8, TINY.hidden), 7.0, dtype=torch.float32, device="cuda")
+    H.hb_run_iteration(dl.layer, [], x, out)
+    bad = [
+        [(0, 0, b.requests[0].block_table)],                        # chunk_len < 1
+        [(5, 10, b.requests[0].block_table[:0])],                   # short table
+        [(5, 10, np.array([99], dtype=np.int32))],                  # id out of range
+        [(5, 10, b.requests[0].block_table), (5, 10, b.requests[0].block_table)],  # same slots
+        [(9, 0, b.requests[0].block_table)],                        # T above capacity
+    ]
+    for reqs in bad:
+        with pytest.raises(H.HBError):
+            H.hb_run_iteration(dl.layer, reqs, x, out)
+    torch.cuda.synchronize()
+    k1, v1 = _pool_bits(dl)
+    np.testing.assert_array_equal(k0, k1)
+    np.testing.assert_array_equal(v0, v1)
+    assert torch.all(out == 7.0)
+
+
+def test_bf16_output_matches_fp32_output(hb):
+    import torch
+    from paper_2503_22562_amd import hb as H
+    from paper_2503_22562_amd.harness import to_device_bf16
+    b = tiny_batch(seed=3)
+    dl, _ = _setup(hb, b)
+    x = to_device_bf16(b.x_in())
+    y32 = dl.run(_reqs(b), x, H.HB_OUT_F32)
+    y16 = dl.run(_reqs(b), x, H.HB_OUT_BF16)
+    torch.cuda.synchronize()
+    ref = y32.to(torch.bfloat16)
+    assert torch.equal(y16, ref)
