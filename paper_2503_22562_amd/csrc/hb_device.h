@@ -16,14 +16,14 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_floa
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// fp32 -> bf16, round to nearest even (inputs are finite)
+// fp32 -> bf16, round to nearest even (the hardware conversion of gfx950)
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return u >> 16;
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+  const bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
@@ -42,5 +42,26 @@ __device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
 }
 
 __device__ __forceinline__ float wave_max_xor(float v, int mask) { return fmaxf(v, __shfl_xor(v, mask, 64)); }
+
+// Load from memory that no kernel of the launch writes (the per-iteration
+// metadata): read through the constant address space so that wave-uniform
+// addresses become scalar loads, which do not wait on outstanding vector
+// memory traffic.
+template <typename T>
+__device__ __forceinline__ T const_load(const T* p) {
+  static_assert(sizeof(T) % 4 == 0, "whole 32-bit words");
+  struct Words {
+    int32_t w[sizeof(T) / 4];
+  } b;
+  const __attribute__((address_space(4))) int32_t* q =
+      reinterpret_cast<const __attribute__((address_space(4))) int32_t*>(reinterpret_cast<uintptr_t>(p));
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 4); ++i) b.w[i] = q[i];
+  return __builtin_bit_cast(T, b);
+}
+
+// Index of the calling wave in its workgroup, as a wave-uniform value (so
+// loads addressed by it become scalar loads).
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
 }  // namespace hb

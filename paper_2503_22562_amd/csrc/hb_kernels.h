@@ -24,7 +24,16 @@ struct GemmArgs {
   const void* R; int ldr; int r_f32;
   int epi;
 };
-void launch_gemm(hipStream_t s, const GemmArgs& a);
+// Tile shape, grid and K split chosen for one GEMM (cfg < 0: the
+// register-staged kernel, used when K is not a multiple of 64).
+struct GemmPlan {
+  int cfg, tiles_m, tiles_n, ksplit, kchunk;
+};
+// force_cfg >= 0 / force_ksplit > 0 restrict the choice to one tile shape /
+// one K split where that split applies (testing).
+GemmPlan plan_gemm(const GemmArgs& a, int cu_count, int force_cfg = -1, int force_ksplit = 0);
+// `partial` holds ksplit * M * N fp32 when plan.ksplit > 1.
+void launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& plan, float* partial);
 
 // Rotate q and k of every batch token at its position and store k and v in the
 // paged pool; q goes to q_out [T][nq*hd].
@@ -51,14 +60,19 @@ struct AttnArgs {
   uint16_t* o;         // [T][nq*hd]
   const uint16_t* k_pool;
   const uint16_t* v_pool;
-  const int32_t* items;
+  const int32_t* tiles;   // workgroup tiles (AttnItem)
+  const int32_t* items;   // wave items (AttnItem)
   int n_items;
+  const int32_t* units;   // per workgroup: tile index, or -1 - (group of 4 items)
+  int n_units;
   const int32_t* groups;
   int n_groups;
+  const int32_t* merge_units;  // per merge workgroup: group * 16 + 16-column block
+  int n_merge_units;
   const int32_t* req_bt;
   const int32_t* bt;
-  float* part_o;   // [parts][16][hd]
-  float* part_ml;  // [parts][16][2]
+  float* part_o;   // [slots][hd]
+  float* part_ml;  // [slots][2]
   int nq, nkv, hd;
   float scale_log2;  // log2(e) / sqrt(hd)
 };

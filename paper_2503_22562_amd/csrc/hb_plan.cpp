@@ -49,6 +49,7 @@ hb_status check_config(const hb_layer_config* c, Dims* d) {
   d->blk = 16;
   d->G = G;
   d->P = 16 / G;
+  d->BQ = 256 / G;
   d->qkv_n = (d->nq + 2 * d->nkv) * d->hd;
   d->theta = c->rope_theta;
   d->eps = c->rms_eps;
@@ -139,7 +140,9 @@ void iteration_work(const Dims& d, const hb_request* reqs, int n, double* flops,
            + T * d.H * 2.0 + T * d.H * 4.0;      // x_in bf16, y fp32
 }
 
-void build_plan(const Dims& d, const hb_batch_desc* desc, int target_items, Plan* p) {
+static int round_up(int64_t x, int m) { return (int)((x + m - 1) / m * m); }
+
+void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p) {
   const int R = desc->n_requests;
   const hb_request* rq = desc->requests;
   int T = 0, nbt = 0;
@@ -147,73 +150,93 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int target_items, Plan
   for (int r = 0; r < R; ++r) {
     tok_start[r] = T;
     T += rq[r].chunk_len;
-    nbt += (int)blocks_for((int64_t)rq[r].context_len + rq[r].chunk_len);
+    nbt += (int)blocks_for((int64_t)rq[r].context_len + rq[r].chunk_len) + kBtPad;
   }
   tok_start[R] = T;
   p->T = T;
   p->R = R;
 
-  // split length: spread the key work over about target_items waves
-  double total_keys = 0;
+  // A chunk that fills at least half a 256-column tile goes to the workgroup
+  // path; decodes and short chunks become 16-column wave items.
+  auto is_tile = [&](int r) { return (int64_t)rq[r].chunk_len * d.G >= 128; };
+  double tile_keys = 0, item_keys = 0;
   for (int r = 0; r < R; ++r) {
-    const int c = rq[r].chunk_len, x = rq[r].context_len;
-    for (int i0 = 0; i0 < c; i0 += d.P) total_keys += (double)d.nkv * (x + std::min(c, i0 + d.P));
+    const int c = rq[r].chunk_len, x = rq[r].context_len, w = is_tile(r) ? d.BQ : d.P;
+    for (int i0 = 0; i0 < c; i0 += w) (is_tile(r) ? tile_keys : item_keys) += (double)d.nkv * (x + std::min(c, i0 + w));
   }
-  int S = (int)std::min<double>(1 << 30, total_keys / std::max(1, target_items));
-  S = std::max(256, (S + 31) & ~31);
-  p->split_len = S;
+  // split lengths (multiples of 64 keys): about one round of tile workgroups
+  // (each split also writes 256 columns of fp32 partials) and about four
+  // items per wave slot (8 per compute unit), so long decodes do not set the
+  // finishing time
+  const int cus = std::max(1, cu_count);
+  const int S_t = std::max(1024, round_up((int64_t)(tile_keys / (1.0 * cus)) + 1, 64));
+  const int S_i = std::max(256, round_up((int64_t)(item_keys / (32.0 * cus)) + 1, 64));
+  p->split_tile = S_t;
+  p->split_item = S_i;
 
-  std::vector<AttnItem> items;
+  std::vector<AttnItem> tiles, items;
   std::vector<MergeGroup> groups;
-  int parts = 0;
+  int slots = 0;
   for (int r = 0; r < R; ++r) {
     const int c = rq[r].chunk_len, x = rq[r].context_len;
-    const int ntiles = (c + d.P - 1) / d.P;
+    const bool tile = is_tile(r);
+    const int w = tile ? d.BQ : d.P, S = tile ? S_t : S_i, ncol = tile ? 256 : 16;
+    std::vector<AttnItem>& out = tile ? tiles : items;
     for (int g = 0; g < d.nkv; ++g) {
-      // splits of the longest tile define the split count of each tile
-      const int kv_max = x + c;
-      const int nsplit_max = (kv_max + S - 1) / S;
-      std::vector<int> part0(ntiles, -1), nspl(ntiles, 1);
-      for (int t = 0; t < ntiles; ++t) {
-        const int i0 = t * d.P, npos = std::min(d.P, c - i0);
+      for (int i0 = 0; i0 < c; i0 += w) {
+        const int npos = std::min(w, c - i0);
         const int kv_len = x + i0 + npos;
-        nspl[t] = (kv_len + S - 1) / S;
-        if (nspl[t] > 1) {
-          part0[t] = parts;
-          groups.push_back({parts, nspl[t], tok_start[r] + i0, npos, g, 0, 0, 0});
-          parts += nspl[t];
+        const int nspl = (kv_len + S - 1) / S;
+        int part0 = -1;
+        if (nspl > 1) {
+          part0 = slots;
+          groups.push_back({slots, nspl, ncol, tok_start[r] + i0, npos, g, 0, 0});
+          slots += nspl * ncol;
         }
-      }
-      for (int s = 0; s < nsplit_max; ++s) {
-        for (int t = 0; t < ntiles; ++t) {
-          if (s >= nspl[t]) continue;
-          const int i0 = t * d.P, npos = std::min(d.P, c - i0);
-          const int kv_len = x + i0 + npos;
-          AttnItem it;
-          it.req = r;
-          it.kv_head = g;
-          it.tok0 = tok_start[r] + i0;
-          it.pos0 = x + i0;
-          it.npos = npos;
-          it.kv_begin = s * S;
-          it.kv_end = std::min(kv_len, (s + 1) * S);
-          it.part = nspl[t] > 1 ? part0[t] + s : -1;
-          items.push_back(it);
-        }
+        for (int s = 0; s < nspl; ++s)
+          out.push_back({r, g, tok_start[r] + i0, x + i0, npos, s * S, std::min(kv_len, (s + 1) * S),
+                         nspl > 1 ? part0 + s * ncol : -1});
       }
     }
   }
+  // longest first (greedy list scheduling over the compute units), and items
+  // of similar length share a workgroup, which lasts as long as its longest
+  auto longer = [](const AttnItem& x, const AttnItem& y) {
+    return (x.kv_end - x.kv_begin) * (int64_t)x.npos > (y.kv_end - y.kv_begin) * (int64_t)y.npos;
+  };
+  std::stable_sort(tiles.begin(), tiles.end(), longer);
+  std::stable_sort(items.begin(), items.end(), [](const AttnItem& x, const AttnItem& y) {
+    return (x.kv_end - x.kv_begin) > (y.kv_end - y.kv_begin);
+  });
+  // work units: one per tile, one per kItemsPerUnit items, interleaved evenly
+  // so that compute-bound and bandwidth-bound workgroups share the GPU
+  const int nt = (int)tiles.size(), ni_units = ((int)items.size() + kItemsPerUnit - 1) / kItemsPerUnit;
+  std::vector<int32_t> units;
+  units.reserve(nt + ni_units);
+  for (int a = 0, b = 0; a < nt || b < ni_units;) {
+    if (b >= ni_units || (a < nt && (int64_t)a * ni_units <= (int64_t)b * nt)) units.push_back(a++);
+    else units.push_back(-1 - b++);
+  }
+  p->n_tiles = nt;
   p->n_items = (int)items.size();
+  p->n_units = (int)units.size();
   p->n_groups = (int)groups.size();
-  p->n_parts = parts;
+  p->n_slots = slots;
+  std::vector<int32_t> merge;
+  for (int gi = 0; gi < p->n_groups; ++gi)
+    for (int cb = 0; cb * 16 < groups[gi].npos * d.G; ++cb) merge.push_back(gi * 16 + cb);
+  p->n_merge_units = (int)merge.size();
 
   int off = 0;
   p->off_tok_pos = off;  off += align16(T);
   p->off_tok_req = off;  off += align16(T);
   p->off_req_bt = off;   off += align16(R);
   p->off_bt = off;       off += align16(nbt);
+  p->off_tiles = off;    off += align16(8 * nt);
   p->off_items = off;    off += align16(8 * p->n_items);
+  p->off_units = off;    off += align16(p->n_units);
   p->off_groups = off;   off += align16(8 * p->n_groups);
+  p->off_merge = off;    off += align16(p->n_merge_units);
   p->meta.assign(off, 0);
   int32_t* m = p->meta.data();
   int bt_off = 0;
@@ -225,10 +248,14 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int target_items, Plan
     m[p->off_req_bt + r] = bt_off;
     const int nb = (int)blocks_for((int64_t)rq[r].context_len + rq[r].chunk_len);
     std::memcpy(m + p->off_bt + bt_off, rq[r].block_table, sizeof(int32_t) * nb);
-    bt_off += nb;
+    for (int i = 0; i < kBtPad; ++i) m[p->off_bt + bt_off + nb + i] = rq[r].block_table[nb - 1];
+    bt_off += nb + kBtPad;
   }
+  if (nt) std::memcpy(m + p->off_tiles, tiles.data(), sizeof(AttnItem) * nt);
   if (!items.empty()) std::memcpy(m + p->off_items, items.data(), sizeof(AttnItem) * items.size());
+  if (!units.empty()) std::memcpy(m + p->off_units, units.data(), sizeof(int32_t) * units.size());
   if (!groups.empty()) std::memcpy(m + p->off_groups, groups.data(), sizeof(MergeGroup) * groups.size());
+  if (!merge.empty()) std::memcpy(m + p->off_merge, merge.data(), sizeof(int32_t) * merge.size());
   iteration_work(d, rq, R, &p->flops, &p->bytes);
 }
 

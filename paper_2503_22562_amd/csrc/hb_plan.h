@@ -21,7 +21,8 @@ const char* last_error();
 struct Dims {
   int H = 0, nq = 0, nkv = 0, hd = 0, F = 0, blk = 16;
   int G = 0;      // q heads per kv head
-  int P = 0;      // query positions per 16-column attention tile = 16 / G
+  int P = 0;      // query positions of a 16-column wave item = 16 / G
+  int BQ = 0;     // query positions of a 256-column workgroup tile = 256 / G
   int qkv_n = 0;  // (nq + 2 nkv) * hd
   float theta = 0.f, eps = 0.f;
   int max_T = 0, max_R = 0;
@@ -29,23 +30,35 @@ struct Dims {
 
 hb_status check_config(const hb_layer_config* cfg, Dims* d);
 
-// One wave of attention work: 16 query columns (P positions x G heads of one
-// kv head) of one request over the key positions [kv_begin, kv_end).
+// Attention work over the key positions [kv_begin, kv_end) of one request
+// and kv head: a wave item covers 16 query columns (P positions x G heads), a
+// workgroup tile 256 columns (BQ positions x G heads). part < 0: the unit
+// writes the normalised output; otherwise its columns' partial results go to
+// column slots part + c.
 struct AttnItem {
-  int32_t req, kv_head, tok0, pos0, npos, kv_begin, kv_end, part;  // part < 0: final
+  int32_t req, kv_head, tok0, pos0, npos, kv_begin, kv_end, part;
 };
-// A tile whose key range was split over `nparts` consecutive partial slots.
+// Columns whose key range was split: part s of column c sits in slot
+// part0 + s * stride + c.
 struct MergeGroup {
-  int32_t part0, nparts, tok0, npos, kv_head, pad0, pad1, pad2;
+  int32_t part0, nparts, stride, tok0, npos, kv_head, pad0, pad1;
 };
 static_assert(sizeof(AttnItem) == 32 && sizeof(MergeGroup) == 32, "packed as 8 int32");
 
+// Each request's block ids are followed by kBtPad copies of its last id, so
+// the four ids of a 64-key step can be read as one vector even at the end.
+constexpr int kBtPad = 3;
+// Wave items are grouped kItemsPerUnit to a workgroup (one per wave).
+constexpr int kItemsPerUnit = 8;
+
 struct Plan {
   int T = 0, R = 0;
-  int n_items = 0, n_groups = 0, n_parts = 0;
-  int split_len = 0;
+  int n_tiles = 0, n_items = 0, n_units = 0, n_groups = 0, n_merge_units = 0;
+  int n_slots = 0;  // partial-result column slots
+  int split_tile = 0, split_item = 0;
   // offsets (int32 units) of each section inside meta
-  int off_tok_pos = 0, off_tok_req = 0, off_req_bt = 0, off_bt = 0, off_items = 0, off_groups = 0;
+  int off_tok_pos = 0, off_tok_req = 0, off_req_bt = 0, off_bt = 0;
+  int off_tiles = 0, off_items = 0, off_units = 0, off_groups = 0, off_merge = 0;
   std::vector<int32_t> meta;
   // algorithmic work of the iteration (for roofline accounting)
   double flops = 0, bytes = 0;
@@ -60,9 +73,8 @@ struct SlotMarks {
 // Validate `desc` against the layer shape and a pool of num_blocks blocks.
 hb_status check_batch(const Dims& d, int num_blocks, const hb_batch_desc* desc, SlotMarks* marks);
 
-// Build the plan of a validated batch. `target_items` steers the split of
-// long key ranges (about the number of waves that fill the GPU).
-void build_plan(const Dims& d, const hb_batch_desc* desc, int target_items, Plan* p);
+// Build the plan of a validated batch for a GPU with cu_count compute units.
+void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p);
 
 // Algorithmic flops and HBM bytes of one iteration (what the method must
 // compute and move, not what an implementation happens to do).

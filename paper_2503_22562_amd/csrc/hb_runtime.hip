@@ -3,6 +3,7 @@
 // profiler.
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -45,6 +46,8 @@ struct hb_layer {
   hb_kv_pool pool{};
   hipStream_t stream = nullptr;
   int device = 0, cu_count = 0;
+  int gemm_tile = -1;   // HB_GEMM_TILE at creation: force one GEMM tile shape (testing)
+  int gemm_ksplit = 0;  // HB_GEMM_KSPLIT at creation: force one K split (testing)
   // workspace
   uint16_t *xn = nullptr, *qkv = nullptr, *q_rot = nullptr, *attn = nullptr, *mlp = nullptr;
   float* h2 = nullptr;
@@ -53,6 +56,8 @@ struct hb_layer {
   int part_cap = 0;
   int32_t* meta = nullptr;
   size_t meta_cap = 0;
+  float* splitk = nullptr;  // split-K partial sums
+  size_t splitk_cap = 0;    // floats
   Stage stage[kStages];
   int stage_next = 0;
   SlotMarks marks;
@@ -80,6 +85,19 @@ hb_status ensure_meta(hb_layer* L, size_t n) {
   return HB_OK;
 }
 
+hb_status ensure_splitk(hb_layer* L, size_t floats) {
+  if (floats <= L->splitk_cap) return HB_OK;
+  HB_HIP(hipStreamSynchronize(L->stream));
+  if (L->splitk) HB_HIP(hipFree(L->splitk));
+  L->splitk = nullptr;
+  L->splitk_cap = 0;
+  if (hipMalloc(&L->splitk, floats * sizeof(float)) != hipSuccess)
+    return fail(HB_ERR_OOM, "split-K workspace of %zu B", floats * 4);
+  L->splitk_cap = floats;
+  return HB_OK;
+}
+
+// Partial-result column slots of split attention work.
 hb_status ensure_parts(hb_layer* L, int n) {
   if (n <= L->part_cap) return HB_OK;
   int cap = std::max(n, L->part_cap * 2);
@@ -88,9 +106,9 @@ hb_status ensure_parts(hb_layer* L, int n) {
   if (L->part_ml) HB_HIP(hipFree(L->part_ml));
   L->part_o = L->part_ml = nullptr;
   L->part_cap = 0;
-  if (hipMalloc(&L->part_o, (size_t)cap * 16 * L->d.hd * sizeof(float)) != hipSuccess ||
-      hipMalloc(&L->part_ml, (size_t)cap * 16 * 2 * sizeof(float)) != hipSuccess)
-    return fail(HB_ERR_OOM, "attention split buffers for %d parts", cap);
+  if (hipMalloc(&L->part_o, (size_t)cap * L->d.hd * sizeof(float)) != hipSuccess ||
+      hipMalloc(&L->part_ml, (size_t)cap * 2 * sizeof(float)) != hipSuccess)
+    return fail(HB_ERR_OOM, "attention split buffers for %d column slots", cap);
   L->part_cap = cap;
   return HB_OK;
 }
@@ -171,7 +189,7 @@ void free_layer(hb_layer* L) {
   if (!L) return;
   (void)hipStreamSynchronize(L->stream);
   for (void* p : {(void*)L->xn, (void*)L->qkv, (void*)L->q_rot, (void*)L->attn, (void*)L->mlp, (void*)L->h2,
-                  (void*)L->inv_freq, (void*)L->part_o, (void*)L->part_ml, (void*)L->meta})
+                  (void*)L->inv_freq, (void*)L->part_o, (void*)L->part_ml, (void*)L->meta, (void*)L->splitk})
     if (p) (void)hipFree(p);
   for (Stage& s : L->stage) {
     if (s.host) (void)hipHostFree(s.host);
@@ -196,26 +214,52 @@ hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
   const Dims& d = L->d;
   Plan& p = L->plan;
   const int T = p.T;
+  hipStream_t s = L->stream;
+  const uint16_t* x_in = static_cast<const uint16_t*>(desc->x_in);
+  GemmArgs gq{}, go{}, gu{}, gd{};
+  gq.A = L->xn; gq.lda = d.H;
+  gq.B = static_cast<const uint16_t*>(L->w.w_qkv); gq.ldb = d.H;
+  gq.M = T; gq.N = d.qkv_n; gq.K = d.H;
+  gq.C = L->qkv; gq.ldc = d.qkv_n; gq.epi = GEMM_STORE_BF16;
+
+  go.A = L->attn; go.lda = d.nq * d.hd;
+  go.B = static_cast<const uint16_t*>(L->w.w_o); go.ldb = d.nq * d.hd;
+  go.M = T; go.N = d.H; go.K = d.nq * d.hd;
+  go.C = L->h2; go.ldc = d.H; go.c_f32 = 1;
+  go.R = x_in; go.ldr = d.H; go.r_f32 = 0; go.epi = GEMM_RESIDUAL;
+
+  gu.A = L->xn; gu.lda = d.H;
+  gu.B = static_cast<const uint16_t*>(L->w.w_gate_up); gu.ldb = d.H;
+  gu.M = T; gu.N = d.F; gu.K = d.H;
+  gu.C = L->mlp; gu.ldc = d.F; gu.epi = GEMM_SWIGLU;
+
+  gd.A = L->mlp; gd.lda = d.F;
+  gd.B = static_cast<const uint16_t*>(L->w.w_down); gd.ldb = d.F;
+  gd.M = T; gd.N = d.H; gd.K = d.F;
+  gd.C = desc->x_out; gd.ldc = d.H; gd.c_f32 = desc->out_dtype == HB_OUT_F32;
+  gd.R = L->h2; gd.ldr = d.H; gd.r_f32 = 1; gd.epi = GEMM_RESIDUAL;
+
+  const GemmPlan pq = plan_gemm(gq, L->cu_count, L->gemm_tile, L->gemm_ksplit),
+                 po = plan_gemm(go, L->cu_count, L->gemm_tile, L->gemm_ksplit);
+  const GemmPlan pu = plan_gemm(gu, L->cu_count, L->gemm_tile, L->gemm_ksplit),
+                 pd = plan_gemm(gd, L->cu_count, L->gemm_tile, L->gemm_ksplit);
+  size_t sk = 0;
+  for (const auto& [pl, ga] : {std::make_pair(pq, gq), std::make_pair(po, go), std::make_pair(pd, gd)})
+    if (pl.ksplit > 1) sk = std::max(sk, (size_t)pl.ksplit * ga.M * ga.N);
+
   hb_status st = ensure_meta(L, p.meta.size());
-  if (st == HB_OK) st = ensure_parts(L, p.n_parts);
+  if (st == HB_OK) st = ensure_parts(L, p.n_slots);
+  if (st == HB_OK) st = ensure_splitk(L, sk);
   if (st != HB_OK) return st;
   st = stage_upload(L, p.meta.data(), p.meta.size(), L->meta);
   if (st != HB_OK) return st;
-  hipStream_t s = L->stream;
   const int32_t* meta = L->meta;
-  const uint16_t* x_in = static_cast<const uint16_t*>(desc->x_in);
 
   st = timed(L, HB_K_RMSNORM_ATTN, [&] {
     launch_rmsnorm(s, x_in, false, static_cast<const uint16_t*>(L->w.g_attn), L->xn, T, d.H, d.eps);
   });
   if (st != HB_OK) return st;
-
-  GemmArgs g{};
-  g.A = L->xn; g.lda = d.H;
-  g.B = static_cast<const uint16_t*>(L->w.w_qkv); g.ldb = d.H;
-  g.M = T; g.N = d.qkv_n; g.K = d.H;
-  g.C = L->qkv; g.ldc = d.qkv_n; g.epi = GEMM_STORE_BF16;
-  st = timed(L, HB_K_GEMM_QKV, [&] { launch_gemm(s, g); });
+  st = timed(L, HB_K_GEMM_QKV, [&] { launch_gemm(s, gq, pq, L->splitk); });
   if (st != HB_OK) return st;
 
   RopeKvArgs r{};
@@ -230,8 +274,11 @@ hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
   AttnArgs at{};
   at.q = L->q_rot; at.o = L->attn;
   at.k_pool = r.k_pool; at.v_pool = r.v_pool;
+  at.tiles = meta + p.off_tiles;
   at.items = meta + p.off_items; at.n_items = p.n_items;
+  at.units = meta + p.off_units; at.n_units = p.n_units;
   at.groups = meta + p.off_groups; at.n_groups = p.n_groups;
+  at.merge_units = meta + p.off_merge; at.n_merge_units = p.n_merge_units;
   at.req_bt = r.req_bt; at.bt = r.bt;
   at.part_o = L->part_o; at.part_ml = L->part_ml;
   at.nq = d.nq; at.nkv = d.nkv; at.hd = d.hd;
@@ -242,42 +289,19 @@ hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
     st = timed(L, HB_K_ATTN_MERGE, [&] { launch_attn_merge(s, at); });
     if (st != HB_OK) return st;
   }
-
-  g = GemmArgs{};
-  g.A = L->attn; g.lda = d.nq * d.hd;
-  g.B = static_cast<const uint16_t*>(L->w.w_o); g.ldb = d.nq * d.hd;
-  g.M = T; g.N = d.H; g.K = d.nq * d.hd;
-  g.C = L->h2; g.ldc = d.H; g.c_f32 = 1;
-  g.R = x_in; g.ldr = d.H; g.r_f32 = 0; g.epi = GEMM_RESIDUAL;
-  st = timed(L, HB_K_GEMM_O, [&] { launch_gemm(s, g); });
+  st = timed(L, HB_K_GEMM_O, [&] { launch_gemm(s, go, po, L->splitk); });
   if (st != HB_OK) return st;
-
   st = timed(L, HB_K_RMSNORM_FFN, [&] {
     launch_rmsnorm(s, L->h2, true, static_cast<const uint16_t*>(L->w.g_ffn), L->xn, T, d.H, d.eps);
   });
   if (st != HB_OK) return st;
-
-  g = GemmArgs{};
-  g.A = L->xn; g.lda = d.H;
-  g.B = static_cast<const uint16_t*>(L->w.w_gate_up); g.ldb = d.H;
-  g.M = T; g.N = d.F; g.K = d.H;
-  g.C = L->mlp; g.ldc = d.F; g.epi = GEMM_SWIGLU;
-  st = timed(L, HB_K_GEMM_GATE_UP, [&] { launch_gemm(s, g); });
+  st = timed(L, HB_K_GEMM_GATE_UP, [&] { launch_gemm(s, gu, pu, L->splitk); });
   if (st != HB_OK) return st;
-
-  g = GemmArgs{};
-  g.A = L->mlp; g.lda = d.F;
-  g.B = static_cast<const uint16_t*>(L->w.w_down); g.ldb = d.F;
-  g.M = T; g.N = d.H; g.K = d.F;
-  g.C = desc->x_out; g.ldc = d.H; g.c_f32 = desc->out_dtype == HB_OUT_F32;
-  g.R = L->h2; g.ldr = d.H; g.r_f32 = 1; g.epi = GEMM_RESIDUAL;
-  st = timed(L, HB_K_GEMM_DOWN, [&] { launch_gemm(s, g); });
+  st = timed(L, HB_K_GEMM_DOWN, [&] { launch_gemm(s, gd, pd, L->splitk); });
   if (st != HB_OK) return st;
   L->last_T = T;
   return check_hip("kernel launch");
 }
-
-int target_items(const hb_layer* L) { return std::max(256, L->cu_count * 16); }
 
 // splitmix64 stream for the profiler's host-side draws
 struct SplitMix {
@@ -326,6 +350,8 @@ hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w,
   hipDeviceProp_t prop;
   if (hipGetDeviceProperties(&prop, L->device) != hipSuccess) return bail(fail(HB_ERR_HIP, "hipGetDeviceProperties failed"));
   L->cu_count = prop.multiProcessorCount;
+  if (const char* e = std::getenv("HB_GEMM_TILE")) L->gemm_tile = std::atoi(e);
+  if (const char* e = std::getenv("HB_GEMM_KSPLIT")) L->gemm_ksplit = std::atoi(e);
   const size_t T = d.max_T;
   struct Alloc { void** p; size_t bytes; } allocs[] = {
       {(void**)&L->xn, T * d.H * 2},         {(void**)&L->qkv, T * d.qkv_n * 2},
@@ -343,7 +369,7 @@ hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w,
     if (hipEventCreateWithFlags(&s.done, hipEventDisableTiming) != hipSuccess)
       return bail(fail(HB_ERR_HIP, "hipEventCreate failed"));
   st = ensure_meta(L, (size_t)1 << 18);
-  if (st == HB_OK) st = ensure_parts(L, 1024);
+  if (st == HB_OK) st = ensure_parts(L, 1 << 16);
   if (st != HB_OK) return bail(st);
   *out = L;
   return HB_OK;
@@ -380,7 +406,7 @@ hb_status hb_run_iteration(hb_layer* L, const hb_batch_desc* desc) {
   hb_status st = check_batch(L->d, L->pool.num_blocks, desc, &L->marks);
   if (st != HB_OK) return st;
   if (desc->n_requests == 0) return HB_OK;
-  build_plan(L->d, desc, target_items(L), &L->plan);
+  build_plan(L->d, desc, L->cu_count, &L->plan);
   return enqueue_layer(L, desc);
 }
 

@@ -1,135 +1,115 @@
 // Varlen paged attention for a hybrid batch: causal chunk rows over their
 // request's cached context and single-token decode rows, in one launch.
 //
-// Work unit = one wavefront = 16 query columns (P = 16/G positions x the G
-// q heads that share one kv head) of one request over a key range. Scores are
-// formed transposed, S^T = K Q^T (16 keys x 16 columns per MFMA), so each lane
-// owns one column and the keys 4*(lane/16)..+3 of a 16-key block: the online
-// softmax rescale is lane-local and only the running maximum needs two
-// cross-lane exchanges per 32 keys. The PV product is also formed transposed,
-// O^T += V^T P^T, with the pool's dim-major V blocks supplying V^T fragments
-// directly and the probabilities reused from the score registers (the MFMA
-// k order only has to agree between its two operands). Long key ranges are
-// split over several waves; a merge kernel combines their partial results
-// with the log-sum-exp rule.
+// Scores are formed transposed, S^T = K Q^T (16 keys x 16 query columns per
+// 16x16x32 MFMA), so a lane owns one query column and keys 4*(lane/16)..+3 of
+// each 16-key block: the online-softmax rescale is lane-local and only the
+// running maximum needs two cross-lane exchanges per step. The PV product is
+// also transposed, O^T += V^T P^T: the probabilities are reused from the score
+// registers (the MFMA k order only has to agree between its two operands) and
+// the pool's V blocks, grouped by four keys and dimension-major inside a
+// group, supply V^T fragments as 8-byte reads. A query column is one
+// (position, q head) pair; the G = n_q / n_kv heads of a kv head sit in
+// adjacent columns so each K/V byte serves all of them.
+//
+// Two kinds of work share the launch, one per 512-thread workgroup (8 waves,
+// two per SIMD, so one wave's softmax arithmetic overlaps the other's MFMAs):
+//  * chunk tiles: 256 columns (8 waves x 32) of one request and kv head over a
+//    key range; 32-key K/V steps (two pool blocks) are copied into a 4-stage
+//    LDS ring by global-to-LDS loads and every wave reads them from there
+//    (K rows XOR-swizzled in 16-byte chunks so fragment reads do not collide
+//    in banks). Compute-bound: 32 MFMAs per wave per step.
+//  * wave items: 16 columns (decodes, short chunks) per wave, eight per
+//    workgroup; each wave streams its K/V straight into registers, the next
+//    32-key step loading while the current one is multiplied. HBM-bound.
+// The planner interleaves the two kinds so compute- and bandwidth-bound
+// workgroups run side by side. Key ranges longer than the split length are
+// divided over several work units; a merge kernel combines their partial
+// results with the log-sum-exp rule.
+#include <algorithm>
+
 #include "hb_device.h"
 #include "hb_kernels.h"
 #include "hb_plan.h"
 
 namespace hb {
+namespace attn_detail {
 
-namespace {
 constexpr float NEG_BIG = -1.0e30f;
+constexpr int WSTEP = 32;   // keys per wave-item step = 2 pool blocks
+constexpr int WAVES = 8;    // waves per workgroup (2 per SIMD)
 
-template <int HD>
-__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int item_id = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (item_id >= a.n_items) return;
-  const AttnItem it = reinterpret_cast<const AttnItem*>(a.items)[item_id];
-  const int G = a.nq / a.nkv;
-  const int col = lane & 15, grp = lane >> 4;
-  const int pi = col / G, hi = col - pi * G;
-  const bool valid = pi < it.npos;
-  const int tok = it.tok0 + pi, pos = it.pos0 + pi;
-  const int g = it.kv_head, h = g * G + hi;
-  const int qstride = a.nq * HD;
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
-  bf16x8 qf[HD / 32];
-#pragma unroll
-  for (int kc = 0; kc < HD / 32; ++kc) {
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (valid) v = ld16(a.q + (size_t)tok * qstride + h * HD + 32 * kc + 8 * grp);
-    qf[kc] = as_bf16x8(v);
-  }
-  const int32_t* btab = a.bt + a.req_bt[it.req];
-  f32x4 o[HD / 16];
-#pragma unroll
-  for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m = NEG_BIG, l = 0.f;
-  const float sc = a.scale_log2;
-  const size_t blk_stride = (size_t)a.nkv * 16 * HD;  // elements per pool block
-  const size_t head_off = (size_t)g * 16 * HD;
+// Online softmax of one column over the N raw scores (q.k) a lane holds for
+// a key step, in log2 units (sc = log2(e)/sqrt(hd)). The running maximum m
+// only moves when some column's step maximum exceeds it by more than
+// RESCALE_SLACK; otherwise the weights 2^(s*sc - m) may reach
+// 2^RESCALE_SLACK, which fp32 accumulation and bf16 weights carry without
+// loss. The result is exact either way (O, l and m change together), and the
+// O rescale -- a read-modify-write of every accumulator -- is mostly skipped.
+// Returns true when the accumulators must be scaled by alpha.
+constexpr float RESCALE_SLACK = 8.0f;
 
-  for (int j0 = it.kv_begin; j0 < it.kv_end; j0 += 32) {
-    const int b0 = btab[j0 >> 4];
-    const bool has1 = j0 + 16 < it.kv_end;
-    const int b1 = has1 ? btab[(j0 >> 4) + 1] : b0;
-    const uint16_t* K0 = a.k_pool + (size_t)b0 * blk_stride + head_off;
-    const uint16_t* K1 = a.k_pool + (size_t)b1 * blk_stride + head_off;
-    const uint16_t* V0 = a.v_pool + (size_t)b0 * blk_stride + head_off;
-    const uint16_t* V1 = a.v_pool + (size_t)b1 * blk_stride + head_off;
-
-    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+template <int N>
+__device__ __forceinline__ bool softmax_step(const float (&sv)[N], float sc, float& m, float& l, float& alpha,
+                                             float (&p)[N]) {
+  float mx = sv[0];
 #pragma unroll
-    for (int kc = 0; kc < HD / 32; ++kc) {
-      const bf16x8 ka = as_bf16x8(ld16(K0 + col * HD + 32 * kc + 8 * grp));
-      const bf16x8 kb = as_bf16x8(ld16(K1 + col * HD + 32 * kc + 8 * grp));
-      s0 = mfma16x16x32(ka, qf[kc], s0);
-      s1 = mfma16x16x32(kb, qf[kc], s1);
-    }
-    // s0[i]: key j0 + 4 grp + i, s1[i]: key j0 + 16 + 4 grp + i, for column `col`
-    float sv[8];
-    const int kbase = j0 + 4 * grp;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int k0i = kbase + i, k1i = kbase + 16 + i;
-      sv[i] = (k0i <= pos && k0i < it.kv_end) ? s0[i] * sc : -INFINITY;
-      sv[4 + i] = (k1i <= pos && k1i < it.kv_end) ? s1[i] * sc : -INFINITY;
-    }
-    float mx = sv[0];
-#pragma unroll
-    for (int i = 1; i < 8; ++i) mx = fmaxf(mx, sv[i]);
-    mx = wave_max_xor(mx, 16);
-    mx = wave_max_xor(mx, 32);
-    const float mn = fmaxf(m, mx);
-    const float alpha = exp2f(m - mn);
-    float pv[8], ps = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      pv[i] = exp2f(sv[i] - mn);
-      ps += pv[i];
-    }
-    l = l * alpha + ps;
+  for (int i = 1; i < N; ++i) mx = fmaxf(mx, sv[i]);
+  mx = wave_max_xor(mx, 16);
+  mx = wave_max_xor(mx, 32);
+  const float ms = mx * sc;  // -inf when every key of the step is masked
+  const bool rescale = __any(ms > m + RESCALE_SLACK);
+  alpha = 1.0f;
+  if (rescale) {
+    const float mn = fmaxf(m, ms);
+    alpha = exp2f(m - mn);
+    l *= alpha;
     m = mn;
-    u32x4 pw = {pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]), pack_bf16x2(pv[4], pv[5]),
-                pack_bf16x2(pv[6], pv[7])};
-    const bf16x8 pf = as_bf16x8(pw);
-    // keys at or past kv_end may be unwritten slots: their V must not reach the MFMA
-    const bool tail = j0 + 32 > it.kv_end;
-#pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt) {
-      const int d = 16 * dt + col;
-      u32x2 va = ld8(V0 + d * 16 + 4 * grp);
-      u32x2 vb = ld8(V1 + d * 16 + 4 * grp);
-      if (tail) {
-#pragma unroll
-        for (int i = 0; i < 4; i += 2) {
-          const int k0i = kbase + i, k1i = kbase + 16 + i;
-          uint32_t ma = (k0i < it.kv_end ? 0xFFFFu : 0u) | (k0i + 1 < it.kv_end ? 0xFFFF0000u : 0u);
-          uint32_t mb = (k1i < it.kv_end ? 0xFFFFu : 0u) | (k1i + 1 < it.kv_end ? 0xFFFF0000u : 0u);
-          va[i >> 1] &= ma;
-          vb[i >> 1] &= mb;
-        }
-      }
-      u32x4 vw = {va[0], va[1], vb[0], vb[1]};
-      o[dt] *= alpha;
-      o[dt] = mfma16x16x32(as_bf16x8(vw), pf, o[dt]);
-    }
   }
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
+  float ps = 0.f;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    p[i] = __builtin_amdgcn_exp2f(fmaf(sv[i], sc, -m));  // no denormal results needed
+    ps += p[i];
+  }
+  l += ps;
+  return rescale;
+}
+
+// P^T operand of keys 32kk..32kk+31: slots 0..3 from block 2kk, 4..7 from 2kk+1.
+template <int N>
+__device__ __forceinline__ bf16x8 p_operand(const float (&p)[N], int kk) {
+  const int a = 8 * kk;
+  u32x4 w = {pack_bf16x2(p[a], p[a + 1]), pack_bf16x2(p[a + 2], p[a + 3]), pack_bf16x2(p[a + 4], p[a + 5]),
+             pack_bf16x2(p[a + 6], p[a + 7])};
+  return as_bf16x8(w);
+}
+
+// Write the result of one column: normalised bf16 output, or fp32 partials.
+template <int HD>
+__device__ __forceinline__ void store_column(const AttnArgs& a, const AttnItem& it, int c, const f32x4 (&o)[HD / 16],
+                                             float m, float l, int grp) {
+  const int G = a.nq / a.nkv;
+  const int pi = c / G;
   if (it.part < 0) {
-    if (!valid) return;
+    if (pi >= it.npos) return;
+    const int h = it.kv_head * G + (c - pi * G);
     const float inv = 1.0f / l;
-    uint16_t* orow = a.o + (size_t)tok * qstride + h * HD + 4 * grp;
+    uint16_t* orow = a.o + (size_t)(it.tok0 + pi) * a.nq * HD + h * HD + 4 * grp;
 #pragma unroll
     for (int dt = 0; dt < HD / 16; ++dt) {
       u32x2 w = {pack_bf16x2(o[dt][0] * inv, o[dt][1] * inv), pack_bf16x2(o[dt][2] * inv, o[dt][3] * inv)};
       st8(orow + 16 * dt, w);
     }
   } else {
-    float* po = a.part_o + ((size_t)it.part * 16 + col) * HD + 4 * grp;
+    const size_t slot = (size_t)it.part + c;
+    float* po = a.part_o + slot * HD + 4 * grp;
 #pragma unroll
     for (int dt = 0; dt < HD / 16; ++dt) {
       u32x4 w = {__float_as_uint(o[dt][0]), __float_as_uint(o[dt][1]), __float_as_uint(o[dt][2]),
@@ -137,50 +117,401 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       st16(po + 16 * dt, w);
     }
     if (grp == 0) {
-      a.part_ml[((size_t)it.part * 16 + col) * 2 + 0] = m;
-      a.part_ml[((size_t)it.part * 16 + col) * 2 + 1] = l;
+      a.part_ml[slot * 2 + 0] = m;
+      a.part_ml[slot * 2 + 1] = l;
     }
   }
 }
 
-// One workgroup per split tile: o = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
+// ---------------------------------------------------------------------------
+// wave item: 16 columns, K/V streamed into registers, one step ahead
+// ---------------------------------------------------------------------------
+template <int HD>
+struct WaveStep {
+  u32x4 k[2][HD / 32];  // per block: the lane's key row, 8 dims of each 32-dim chunk
+  u32x2 v[2][HD / 16];  // per block: 4 keys of one dim per 16-dim tile
+};
+
+template <int HD>
+__device__ __forceinline__ void wave_load(WaveStep<HD>& st, const AttnArgs& a, int id0, int id1, int g, int col,
+                                          int grp) {
+  const size_t blk_stride = (size_t)a.nkv * 16 * HD;
+  const size_t head_off = (size_t)g * 16 * HD;
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int id = b ? id1 : id0;
+    const uint16_t* K = a.k_pool + (size_t)id * blk_stride + head_off;
+    const uint16_t* V = a.v_pool + (size_t)id * blk_stride + head_off;
+#pragma unroll
+    for (int kc = 0; kc < HD / 32; ++kc) st.k[b][kc] = ld16(K + col * HD + 32 * kc + 8 * grp);
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) st.v[b][dt] = ld8(V + (grp * HD + 16 * dt + col) * 4);
+  }
+}
+
+template <int HD>
+__device__ __forceinline__ void wave_compute(const WaveStep<HD>& st, int j0, const AttnItem& it, int pos, int grp,
+                                             float sc, const bf16x8 (&qf)[HD / 32], f32x4 (&o)[HD / 16], float& m,
+                                             float& l) {
+  f32x4 s[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kc = 0; kc < HD / 32; ++kc) s[b] = mfma16x16x32(as_bf16x8(st.k[b][kc]), qf[kc], s[b]);
+  }
+  float sv[8], p[8];
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sv[4 * b + i] = s[b][i];
+  if (j0 + WSTEP > it.kv_end || j0 + WSTEP > it.pos0) {  // causal / tail masking (wave-uniform)
+    const int lim = min(pos, it.kv_end - 1);
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (j0 + 16 * b + 4 * grp + i > lim) sv[4 * b + i] = -INFINITY;
+  }
+  float alpha;
+  const bool rescale = softmax_step<8>(sv, sc, m, l, alpha, p);
+  const bf16x8 pf = p_operand(p, 0);
+  // keys at or past kv_end may be unwritten slots holding non-finite bits
+  // (0 * NaN would poison the sum): their V lanes are cleared
+  uint32_t vm[2][2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int k0 = j0 + 16 * b + 4 * grp;
+    vm[b][0] = (k0 < it.kv_end ? 0xFFFFu : 0u) | (k0 + 1 < it.kv_end ? 0xFFFF0000u : 0u);
+    vm[b][1] = (k0 + 2 < it.kv_end ? 0xFFFFu : 0u) | (k0 + 3 < it.kv_end ? 0xFFFF0000u : 0u);
+  }
+#pragma unroll
+  for (int dt = 0; dt < HD / 16; ++dt) {
+    u32x2 v0 = st.v[0][dt], v1 = st.v[1][dt];
+    v0[0] &= vm[0][0]; v0[1] &= vm[0][1];
+    v1[0] &= vm[1][0]; v1[1] &= vm[1][1];
+    if (rescale) o[dt] *= alpha;
+    o[dt] = mfma16x16x32(as_bf16x8(u32x4{v0[0], v0[1], v1[0], v1[1]}), pf, o[dt]);
+  }
+}
+
+template <int HD>
+__device__ __forceinline__ void wave_item(const AttnArgs& a, const AttnItem& it, int lane) {
+  const int G = a.nq / a.nkv;
+  const int col = lane & 15, grp = lane >> 4;
+  const int pi = col / G;
+  const bool valid = pi < it.npos;
+  const int pos = it.pos0 + pi;
+  const int g = it.kv_head, h = g * G + (col - pi * G);
+  bf16x8 qf[HD / 32];
+#pragma unroll
+  for (int kc = 0; kc < HD / 32; ++kc) {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (valid) v = ld16(a.q + (size_t)(it.tok0 + pi) * a.nq * HD + h * HD + 32 * kc + 8 * grp);
+    qf[kc] = as_bf16x8(v);
+  }
+  const int32_t* btab = a.bt + const_load(a.req_bt + it.req);
+  const int kb_last = (it.kv_end - 1) >> 4;
+  f32x4 o[HD / 16];
+#pragma unroll
+  for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m = NEG_BIG, l = 0.f;
+  const int nsteps = (it.kv_end - it.kv_begin + WSTEP - 1) / WSTEP;
+  // the table is padded with copies of its last id (kBtPad), so the two ids
+  // of a step are one 8-byte read; steps past the end re-read the last block
+  typedef int32_t i32x2 __attribute__((ext_vector_type(2)));
+  auto ids_of = [&](int s) {
+    return const_load(reinterpret_cast<const i32x2*>(btab + min((it.kv_begin >> 4) + 2 * s, kb_last)));
+  };
+  // Block ids are fetched one step before the loads that use them. Loads in
+  // the steady-state loop are unconditional so the compiler can wait for one
+  // step's registers while the next step's loads stay in flight; the last
+  // one or two steps are peeled off.
+  WaveStep<HD> A, B;
+  i32x2 ids = ids_of(0);
+  wave_load(A, a, ids[0], ids[1], g, col, grp);
+  ids = ids_of(1);
+  int s = 0;
+  for (; s + 2 < nsteps; s += 2) {
+    wave_load(B, a, ids[0], ids[1], g, col, grp);
+    ids = ids_of(s + 2);
+    __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the compute
+    wave_compute(A, it.kv_begin + WSTEP * s, it, pos, grp, a.scale_log2, qf, o, m, l);
+    __builtin_amdgcn_sched_barrier(0);
+    wave_load(A, a, ids[0], ids[1], g, col, grp);
+    ids = ids_of(s + 3);
+    __builtin_amdgcn_sched_barrier(0);
+    wave_compute(B, it.kv_begin + WSTEP * (s + 1), it, pos, grp, a.scale_log2, qf, o, m, l);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (s + 1 < nsteps) {
+    wave_load(B, a, ids[0], ids[1], g, col, grp);
+    wave_compute(A, it.kv_begin + WSTEP * s, it, pos, grp, a.scale_log2, qf, o, m, l);
+    wave_compute(B, it.kv_begin + WSTEP * (s + 1), it, pos, grp, a.scale_log2, qf, o, m, l);
+  } else {
+    wave_compute(A, it.kv_begin + WSTEP * s, it, pos, grp, a.scale_log2, qf, o, m, l);
+  }
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  store_column<HD>(a, it, col, o, m, l, grp);
+}
+
+// ---------------------------------------------------------------------------
+// chunk tile: 256 columns, K/V staged in an LDS ring by the DMA path
+// ---------------------------------------------------------------------------
+constexpr int TSTEP = 32;    // keys per tile step = 2 pool blocks
+constexpr int TSTAGES = 4;   // LDS ring depth of the tile path
+
+template <int HD>
+struct TileGeom {
+  static constexpr int BLK = 16 * HD * 2;        // bytes of one block of one head
+  static constexpr int STAGE = 4 * BLK;          // 2 K blocks then 2 V blocks
+  static constexpr int ROW = HD * 2;             // bytes of one key row
+  static constexpr int LOADS = BLK / 1024;       // 1-KB loads per block
+  static constexpr int KEYS_PER_LOAD = 1024 / ROW;
+  static constexpr int CHUNKS = ROW / 16;        // 16-byte chunks per key row
+};
+
+// One step is four blocks in the stage: K of the two pool blocks (rows
+// XOR-swizzled by 16-byte chunk), then their V (verbatim). Waves 2b and 2b+1
+// copy block b, each half of its 1-KB loads.
+template <int HD>
+__device__ __forceinline__ void tile_issue(uint8_t* stage, const AttnArgs& a, int id, int g, int wave, int lane) {
+  using TG = TileGeom<HD>;
+  constexpr int HALF = TG::LOADS / 2;
+  const int b = wave >> 1, i0 = (wave & 1) * HALF;
+  const size_t blk_stride = (size_t)a.nkv * 16 * HD;
+  const size_t off = (size_t)id * blk_stride + (size_t)g * 16 * HD;
+  uint8_t* dst = stage + b * TG::BLK;
+  if (b < 2) {
+    const uint16_t* K = a.k_pool + off;
+    const int kk_lane = lane / TG::CHUNKS, pc = lane % TG::CHUNKS;
+#pragma unroll
+    for (int j = 0; j < HALF; ++j) {
+      const int i = i0 + j;
+      const int kk = i * TG::KEYS_PER_LOAD + kk_lane;
+      __builtin_amdgcn_global_load_lds(K + kk * HD + 8 * (pc ^ (kk & 7)), dst + i * 1024, 16, 0, 0);
+    }
+  } else {
+    const uint8_t* V = reinterpret_cast<const uint8_t*>(a.v_pool + off);
+#pragma unroll
+    for (int j = 0; j < HALF; ++j) {
+      const int i = i0 + j;
+      __builtin_amdgcn_global_load_lds(V + i * 1024 + lane * 16, dst + i * 1024, 16, 0, 0);
+    }
+  }
+}
+
+template <int HD>
+__device__ __forceinline__ void tile_unit(const AttnArgs& a, const AttnItem& it, uint8_t* smem) {
+  using TG = TileGeom<HD>;
+  constexpr int KC = HD / 32, DT = HD / 16;
+  constexpr int CT = 2;  // 16-column tiles per wave (8 waves x 32 columns)
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
+  const int G = a.nq / a.nkv;
+  const int col = lane & 15, grp = lane >> 4;
+  const int g = it.kv_head;
+  bf16x8 qf[CT][KC];
+  int pos[CT];
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct) {
+    const int c = 32 * wave + 16 * ct + col;
+    const int pi = c / G;
+    const bool valid = pi < it.npos;
+    pos[ct] = it.pos0 + pi;
+    const int h = g * G + (c - pi * G);
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (valid) v = ld16(a.q + (size_t)(it.tok0 + pi) * a.nq * HD + h * HD + 32 * kc + 8 * grp);
+      qf[ct][kc] = as_bf16x8(v);
+    }
+  }
+  const int32_t* btab = a.bt + const_load(a.req_bt + it.req);
+  const int kb_last = (it.kv_end - 1) >> 4;
+  const int kb0 = it.kv_begin >> 4;
+  const int nsteps = (it.kv_end - it.kv_begin + TSTEP - 1) / TSTEP;
+  // pool block of step s copied by this wave (stage block wave/2 holds the K
+  // of pool block 0, 1 or the V of pool block 0, 1)
+  auto block_id = [&](int s) { return const_load(btab + min(kb0 + 2 * s + ((wave >> 1) & 1), kb_last)); };
+
+  f32x4 o[CT][DT];
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[ct][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m[CT], l[CT];
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct) { m[ct] = NEG_BIG; l[ct] = 0.f; }
+
+  const int k_lane = col * TG::ROW;
+  const int v_lane = ((grp * HD + col) * 4) * 2;
+  int next_id = block_id(0);
+#pragma unroll
+  for (int s0 = 0; s0 < TSTAGES - 1; ++s0) {
+    if (s0 < nsteps) tile_issue<HD>(smem + s0 * TG::STAGE, a, next_id, g, wave, lane);
+    if (s0 + 1 < nsteps) next_id = block_id(s0 + 1);
+  }
+  for (int kt = 0; kt < nsteps; ++kt) {
+    // this wave's loads of step kt are complete once at most those of the
+    // (up to TSTAGES - 2) later steps already issued are pending
+    const int ahead = min(TSTAGES - 2, nsteps - 1 - kt);
+    if (ahead >= 2) wait_vmcnt<2 * (TG::LOADS / 2)>();
+    else if (ahead == 1) wait_vmcnt<TG::LOADS / 2>();
+    else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    const int j0 = it.kv_begin + TSTEP * kt;
+    uint8_t* st = smem + (kt % TSTAGES) * TG::STAGE;
+    if (j0 + TSTEP > it.kv_end) {
+      // clear V of keys past kv_end (unwritten slots may hold non-finite bits)
+      for (int e = tid; e < 2 * 16 * HD; e += 64 * WAVES) {
+        const int b = e / (16 * HD), r = e % (16 * HD), key = r / HD, d = r % HD;
+        if (j0 + 16 * b + key >= it.kv_end)
+          reinterpret_cast<uint16_t*>(st + 2 * TG::BLK + b * TG::BLK)[((key >> 2) * HD + d) * 4 + (key & 3)] = 0;
+      }
+      __syncthreads();
+    }
+    if (kt + TSTAGES - 1 < nsteps) {
+      tile_issue<HD>(smem + ((kt + TSTAGES - 1) % TSTAGES) * TG::STAGE, a, next_id, g, wave, lane);
+      if (kt + TSTAGES < nsteps) next_id = block_id(kt + TSTAGES);
+    }
+    // S^T = K Q^T: all K fragment reads first so LDS latency is paid once
+    bf16x8 kf[2][KC];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+        kf[b][kc] = as_bf16x8(*reinterpret_cast<const u32x4*>(st + b * TG::BLK + k_lane + (((4 * kc + grp) ^ (col & 7)) << 4)));
+    __builtin_amdgcn_sched_barrier(0);
+    f32x4 sc[CT][2];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        sc[ct][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc) sc[ct][b] = mfma16x16x32(kf[b][kc], qf[ct][kc], sc[ct][b]);
+      }
+    // V^T fragments (keys 4 grp..+3 of both blocks), read while the softmax runs
+    const uint8_t* vs = st + 2 * TG::BLK + v_lane;
+    bf16x8 vf[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const u32x2 va = *reinterpret_cast<const u32x2*>(vs + dt * 128);
+      const u32x2 vb = *reinterpret_cast<const u32x2*>(vs + TG::BLK + dt * 128);
+      vf[dt] = as_bf16x8(u32x4{va[0], va[1], vb[0], vb[1]});
+    }
+    const bool masked = (j0 + TSTEP > it.kv_end) || (j0 + TSTEP > it.pos0);  // wave-uniform
+    bf16x8 pf[CT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+      float sv[8], p[8];
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sv[4 * b + i] = sc[ct][b][i];
+      if (masked) {
+        const int lim = min(pos[ct], it.kv_end - 1);
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (j0 + 16 * b + 4 * grp + i > lim) sv[4 * b + i] = -INFINITY;
+      }
+      float alpha;
+      if (softmax_step<8>(sv, a.scale_log2, m[ct], l[ct], alpha, p)) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[ct][dt] *= alpha;
+      }
+      pf[ct] = p_operand(p, 0);
+    }
+    // O^T += V^T P^T
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) o[ct][dt] = mfma16x16x32(vf[dt], pf[ct], o[ct][dt]);
+  }
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct) {
+    float lt = l[ct];
+    lt += __shfl_xor(lt, 16, 64);
+    lt += __shfl_xor(lt, 32, 64);
+    store_column<HD>(a, it, 32 * wave + 16 * ct + col, o[ct], m[ct], lt, grp);
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(64 * WAVES, 1) void attn_kernel(AttnArgs a) {
+  extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
+  const int unit = const_load(a.units + blockIdx.x);
+  if (unit >= 0) {
+    tile_unit<HD>(a, const_load(reinterpret_cast<const AttnItem*>(a.tiles) + unit), smem);
+  } else {
+    const int idx = (-unit - 1) * WAVES + wave_id();
+    if (idx < a.n_items)
+      wave_item<HD>(a, const_load(reinterpret_cast<const AttnItem*>(a.items) + idx), threadIdx.x & 63);
+  }
+}
+
+// Merge of split work: one workgroup per (merge group, 16 columns), one
+// thread per (column, 8 dims), folding the parts in order with the online
+// rule: M' = max(M, m_s), acc' = acc 2^(M-M') + O_s 2^(m_s-M'), likewise L.
 template <int HD>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-  const MergeGroup gr = reinterpret_cast<const MergeGroup*>(a.groups)[blockIdx.x];
+  const int mu = const_load(a.merge_units + blockIdx.x);
+  const MergeGroup gr = const_load(reinterpret_cast<const MergeGroup*>(a.groups) + (mu >> 4));
   const int G = a.nq / a.nkv;
-  const int ncol = gr.npos * G;
-  const int qstride = a.nq * HD;
-  for (int idx = threadIdx.x; idx < ncol * (HD / 4); idx += 256) {
-    const int c = idx / (HD / 4), d = (idx - c * (HD / 4)) * 4;
-    float M = NEG_BIG;
-    for (int s = 0; s < gr.nparts; ++s) M = fmaxf(M, a.part_ml[((size_t)(gr.part0 + s) * 16 + c) * 2]);
-    float L = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < gr.nparts; ++s) {
-      const size_t pc = (size_t)(gr.part0 + s) * 16 + c;
-      const float w = exp2f(a.part_ml[pc * 2] - M);
-      L += w * a.part_ml[pc * 2 + 1];
-      const u32x4 v = ld16(a.part_o + pc * HD + d);
-      for (int j = 0; j < 4; ++j) acc[j] += w * __uint_as_float(v[j]);
+  constexpr int TPC = HD / 8;  // threads per column
+  const int c = (mu & 15) * 16 + threadIdx.x / TPC;
+  if (threadIdx.x >= 16 * TPC || c >= gr.npos * G) return;
+  const int d = (threadIdx.x % TPC) * 8;
+  float M = NEG_BIG, L = 0.f, acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < gr.nparts; ++s) {
+    const size_t slot = (size_t)gr.part0 + (size_t)s * gr.stride + c;
+    const u32x2 ml = ld8(a.part_ml + slot * 2);
+    const float ms = __uint_as_float(ml[0]), ls = __uint_as_float(ml[1]);
+    const u32x4 o0 = ld16(a.part_o + slot * HD + d), o1 = ld16(a.part_o + slot * HD + d + 4);
+    const float Mn = fmaxf(M, ms);
+    const float wa = exp2f(M - Mn), wb = exp2f(ms - Mn);
+    L = L * wa + ls * wb;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      acc[j] = acc[j] * wa + __uint_as_float(o0[j]) * wb;
+      acc[4 + j] = acc[4 + j] * wa + __uint_as_float(o1[j]) * wb;
     }
-    const float inv = 1.0f / L;
-    const int pi = c / G, h = gr.kv_head * G + (c - pi * G);
-    u32x2 w = {pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv)};
-    st8(a.o + (size_t)(gr.tok0 + pi) * qstride + h * HD + d, w);
+    M = Mn;
   }
+  const float inv = 1.0f / L;
+  const int pi = c / G, h = gr.kv_head * G + (c - pi * G);
+  u32x4 w = {pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
+             pack_bf16x2(acc[4] * inv, acc[5] * inv), pack_bf16x2(acc[6] * inv, acc[7] * inv)};
+  st16(a.o + (size_t)(gr.tok0 + pi) * a.nq * HD + h * HD + d, w);
 }
-}  // namespace
+
+template <int HD>
+void launch(hipStream_t s, const AttnArgs& a) {
+  constexpr int lds = TSTAGES * TileGeom<HD>::STAGE;
+  static bool attr = false;
+  if (!attr) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<HD>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    attr = true;
+  }
+  attn_kernel<HD><<<a.n_units, 64 * WAVES, lds, s>>>(a);
+}
+
+}  // namespace attn_detail
 
 void launch_attention(hipStream_t s, const AttnArgs& a) {
-  if (a.n_items <= 0) return;
-  const int grid = (a.n_items + 3) / 4;
-  if (a.hd == 128) attn_kernel<128><<<grid, 256, 0, s>>>(a);
-  else attn_kernel<64><<<grid, 256, 0, s>>>(a);
+  if (a.n_units <= 0) return;
+  if (a.hd == 128) attn_detail::launch<128>(s, a);
+  else attn_detail::launch<64>(s, a);
 }
 
 void launch_attn_merge(hipStream_t s, const AttnArgs& a) {
-  if (a.n_groups <= 0) return;
-  if (a.hd == 128) attn_merge_kernel<128><<<a.n_groups, 256, 0, s>>>(a);
-  else attn_merge_kernel<64><<<a.n_groups, 256, 0, s>>>(a);
+  if (a.n_merge_units <= 0) return;
+  if (a.hd == 128) attn_detail::attn_merge_kernel<128><<<a.n_merge_units, 256, 0, s>>>(a);
+  else attn_detail::attn_merge_kernel<64><<<a.n_merge_units, 256, 0, s>>>(a);
 }
 
 }  // namespace hb

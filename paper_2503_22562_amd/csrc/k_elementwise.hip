@@ -71,7 +71,7 @@ void launch_rmsnorm(hipStream_t s, const void* x, bool x_f32, const uint16_t* g,
 // ---------------------------------------------------------------------------
 // RoPE + KV scatter: one workgroup per token. Angles p * theta^(-2j/hd) are
 // formed and evaluated in fp64, then rounded to fp32 for the rotation.
-// K goes to k_pool[blk][g][slot][d], V to v_pool[blk][g][d][slot].
+// K goes to k_pool[blk][g][slot][d], V to v_pool[blk][g][slot/4][d][slot%4].
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
   __shared__ float cs[64], sn[64];
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
   const uint16_t* vrow = krow + a.nkv * hd;
   for (int idx = tid; idx < a.nkv * hd; idx += 256) {
     const int g = idx / hd, d = idx - g * hd;
-    a.v_pool[(((size_t)blk * a.nkv + g) * hd + d) * 16 + slot] = vrow[idx];
+    a.v_pool[((size_t)blk * a.nkv + g) * 16 * hd + ((slot >> 2) * hd + d) * 4 + (slot & 3)] = vrow[idx];
   }
 }
 
@@ -131,7 +131,7 @@ __global__ __launch_bounds__(256) void append_kv_kernel(const uint16_t* __restri
   for (int idx = threadIdx.x; idx < n; idx += 256) {
     const int g = idx / hd, d = idx - g * hd;
     k_pool[(((size_t)blk * nkv + g) * 16 + slot) * hd + d] = k[(size_t)t * n + idx];
-    v_pool[(((size_t)blk * nkv + g) * hd + d) * 16 + slot] = v[(size_t)t * n + idx];
+    v_pool[((size_t)blk * nkv + g) * 16 * hd + ((slot >> 2) * hd + d) * 4 + (slot & 3)] = v[(size_t)t * n + idx];
   }
 }
 

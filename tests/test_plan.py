@@ -1,0 +1,110 @@
+"""The host planner of hb_run_iteration (paper_2503_22562_amd/csrc/hb_plan.cpp,
+no HIP), built with g++ against a small driver: every query row of every
+request and kv head must see each key of [0, position] in exactly one work
+unit, with key ranges on the 64-key step grid, and split results must land
+in disjoint partial slots."""
+import os
+import subprocess
+from collections import defaultdict
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2503_22562_amd", "csrc")
+
+
+@pytest.fixture(scope="module")
+def driver(tmp_path_factory):
+    exe = str(tmp_path_factory.mktemp("plan") / "plan_driver")
+    cmd = ["g++", "-O1", "-std=c++17", f"-I{CSRC}", f"-I{os.path.join(ROOT, 'include')}",
+           os.path.join(ROOT, "tests", "plan_driver.cpp"), os.path.join(CSRC, "hb_plan.cpp"), "-o", exe]
+    subprocess.run(cmd, check=True)
+    return exe
+
+
+def run_plan(exe, shape, cu, reqs):
+    H, nq, nkv, hd, F = shape
+    lines = [f"{H} {nq} {nkv} {hd} {F} {cu} {len(reqs)}"]
+    nxt = 0
+    for c, x in reqs:
+        nb = -(-(c + x) // 16)
+        lines.append(f"{c} {x} {nb} " + " ".join(str(nxt + i) for i in range(nb)))
+        nxt += nb
+    out = subprocess.run([exe], input="\n".join(lines) + "\n", capture_output=True, text=True, check=True).stdout
+    plan = defaultdict(list)
+    for ln in out.splitlines():
+        k, *v = ln.split()
+        plan[k].append([int(t) for t in v])
+    return plan
+
+
+def check(plan, shape, reqs):
+    H, nq, nkv, hd, F = shape
+    G = nq // nkv
+    starts = np.concatenate([[0], np.cumsum([c for c, _ in reqs])])
+    tok_req = np.repeat(np.arange(len(reqs)), [c for c, _ in reqs])
+    # token metadata
+    toks = plan["tok"]
+    assert len(toks) == starts[-1]
+    for t, (pos, r) in enumerate(toks):
+        assert r == tok_req[t] and pos == reqs[r][1] + t - starts[r]
+    assert all(o[0] % 16 == 0 for o in plan["off"])
+    # coverage: (token, kv head) -> list of key ranges
+    cover = defaultdict(list)
+    slots = []
+    for kind, width in (("tile", 256), ("item", 16)):
+        for req, g, tok0, pos0, npos, kb, ke, part in plan[kind]:
+            assert kb % 64 == 0 and kb < ke and npos * G <= width
+            assert tok0 == starts[req] + pos0 - reqs[req][1]
+            assert ke <= pos0 + npos and ke <= reqs[req][0] + reqs[req][1]
+            for i in range(npos):
+                cover[(tok0 + i, g)].append((kb, ke, part))
+            if part >= 0:
+                slots.append((part, part + width))
+    for t in range(starts[-1]):
+        pos = toks[t][0]
+        for g in range(nkv):
+            rng = sorted(cover[(t, g)])
+            assert rng, f"token {t} head {g} not covered"
+            assert rng[0][0] == 0
+            for (a0, a1, _), (b0, b1, _) in zip(rng, rng[1:]):
+                assert a1 == b0, f"token {t} head {g}: gap or overlap {rng}"
+            assert rng[-1][1] >= pos + 1
+            # a later split of a tile may hold only keys past this row's position:
+            # the row then contributes l = 0 to the merge, which drops it
+            assert (len(rng) == 1) == (rng[0][2] < 0)
+    slots.sort()
+    for (a0, a1), (b0, b1) in zip(slots, slots[1:]):
+        assert a1 <= b0, "partial slots overlap"
+    # merge groups and their 16-column merge units
+    want = []
+    for gi, (p0, n, stride, tok0, npos, g, _, _) in enumerate(plan["group"]):
+        assert n > 1 and stride in (16, 256) and npos * G <= stride
+        want += [gi * 16 + cb for cb in range(-(-npos * G // 16))]
+    assert sorted(u[0] for u in plan["merge"]) == want
+    # units: each tile once, each group of eight items once
+    units = [u[0] for u in plan["unit"]]
+    tiles = sorted(u for u in units if u >= 0)
+    groups = sorted(-1 - u for u in units if u < 0)
+    assert tiles == list(range(len(plan["tile"])))
+    assert groups == list(range(-(-len(plan["item"]) // 8)))
+
+
+SHAPES = {"tiny": (256, 4, 2, 64, 688), "8b": (4096, 32, 8, 128, 14336), "70b": (8192, 64, 8, 128, 28672),
+          "g16": (1024, 16, 1, 64, 512), "g1": (512, 4, 4, 128, 336)}
+
+
+@pytest.mark.parametrize("name,reqs,cu", [
+    ("tiny", [(64, 128)] + [(1, 256)] * 8, 256),
+    ("8b", [(512, 3431)] + [(1, int(c)) for c in np.linspace(512, 4096, 64)], 256),
+    ("8b", [(2048, 0)], 256),
+    ("8b", [(128, 0)] + [(1, int(c)) for c in np.geomspace(256, 8192, 256)], 256),
+    ("70b", [(2048, 30720)] + [(1, 32768)] * 32, 256),
+    ("g16", [(37, 21), (1, 0), (300, 5), (5, 3)], 8),
+    ("g1", [(129, 0), (1, 15), (1, 16), (7, 1000)], 4),
+    ("8b", [(33, 0), (32, 40), (31, 1)], 1),
+])
+def test_plan_covers_every_key_once(driver, name, reqs, cu):
+    plan = run_plan(driver, SHAPES[name], cu, reqs)
+    check(plan, SHAPES[name], reqs)
