@@ -82,20 +82,30 @@ TRAFFIC_SOURCES = {
 
 
 def measured_traffic(kernel, workload):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, only
-    if the kernel's sources are unchanged since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    """HBM bytes per launch from the committed rocprofv3 counter summary
+    (profiles/traffic_<kernel>_<workload>.txt, `key: value` lines), only if the
+    kernel's sources are unchanged since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
     if not os.path.exists(path) or kernel not in TRAFFIC_SOURCES:
         return None
+    rec = {}
     with open(path) as f:
-        rec = json.load(f)
+        for line in f:
+            if ":" in line and not line.startswith((" ", "#", "|")):
+                k, v = line.split(":", 1)
+                rec[k.strip()] = v.strip()
     if rec.get("sources_digest") != kernel_sources_digest(TRAFFIC_SOURCES[kernel]):
         return None
-    return rec.get("bytes_per_launch")
+    try:
+        return float(rec["bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
-def cpu_baseline(batch, weights_bits, budget_s=20.0):
-    """The oracle (fp64 NumPy) on the same batch, host cores, timed."""
+def cpu_baseline(batch, weights_bits, min_cpu_s=10.0, max_wall_s=40.0):
+    """The oracle (fp64 NumPy) on the same batch, host cores, timed. The
+    batch is run repeatedly until at least min_cpu_s of oracle time has been
+    measured (seeding each run's cached context is not timed)."""
     import oracle
     shape = batch.shape
     w64 = oracle.weights_to_f64(weights_bits)
@@ -111,7 +121,7 @@ def cpu_baseline(batch, weights_bits, budget_s=20.0):
         t0 = time.perf_counter()
         oracle.layer_forward(w64, shape, cache, batch.requests, x)
         times.append(time.perf_counter() - t0)
-        if time.perf_counter() - t_start > budget_s or len(times) >= 3:
+        if sum(times) >= min_cpu_s or time.perf_counter() - t_start > max_wall_s:
             break
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
     try:
@@ -119,10 +129,27 @@ def cpu_baseline(batch, weights_bits, budget_s=20.0):
         threads = max(int(i.get("num_threads", 0)) for i in threadpool_info()) or threads
     except Exception:
         pass
-    t = float(np.median(times))
-    return {"value": batch.n_tokens / t, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"whole batch ({batch.n_tokens} tokens, {len(batch.requests)} requests), fp64 NumPy oracle, "
-                      f"median of {len(times)} runs of {t:.2f} s; cached-context seeding not timed"}
+    total = float(sum(times))
+    return {"value": batch.n_tokens * len(times) / total, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"the bench batch ({batch.n_tokens} tokens, {len(batch.requests)} requests) run "
+                      f"{len(times)} times, {total:.1f} s of fp64 NumPy oracle time; "
+                      f"cached-context seeding not timed"}
+
+
+def copy_calibration(nbytes=1 << 30, reps=3):
+    """A plain device copy of known size: nbytes read and nbytes written per
+    launch. Profiling it with the same counters as the kernels gives the
+    factor between what FETCH_SIZE / WRITE_SIZE report and the bytes moved."""
+    import torch
+    torch.cuda.set_device(0)
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "launches": reps}), flush=True)
+    return 0
 
 
 def main() -> int:
@@ -133,11 +160,15 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--profile-iters", type=int, default=15)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy (counter calibration) and exit")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the hybrid-batch layer runs on a single MI355X; "
               "run it with --gpus 1.", file=sys.stderr)
         return 2
+    if a.copy_calibration:
+        return copy_calibration()
 
     import torch
     from hb_workloads import LLAMA3_8B, POOL_TOKENS, SWEEP_CHUNKS, SWEEP_DECODES, llama8b_batch, make_weights, \
@@ -166,21 +197,41 @@ def main() -> int:
         dl.run(reqs, x, hb.HB_OUT_F32, y)
     torch.cuda.synchronize()
 
-    # timed region: exactly `steps` iterations, per-kernel HIP events on the layer's stream
+    work = kernel_work(shape, [(c, xx) for c, xx, _ in reqs])
+
+    # per-kernel breakdown (every launch bracketed by events) picks the dominant kernel
     hb.hb_set_kernel_timing(dl.layer, True)
     hb.hb_kernel_times(dl.layer, reset=True)
+    for _ in range(a.steps):
+        dl.run(reqs, x, hb.HB_OUT_F32, y)
+    breakdown = hb.hb_kernel_times(dl.layer, reset=True)
+    hb.hb_set_kernel_timing(dl.layer, False)
+    kernels = {}
+    for name, (tot, n) in breakdown.items():
+        if n == 0:
+            continue
+        avg_ms = tot / n
+        fl, by = work.get(name, (0.0, 0.0))
+        kernels[name] = {"avg_ms": round(avg_ms, 5), "launches": n,
+                         "tflops": round(fl / (avg_ms * 1e-3) / 1e12, 2) if fl else None,
+                         "gbps": round(by / (avg_ms * 1e-3) / 1e9, 1) if by else None}
+    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
+
+    # timed region: exactly `steps` iterations; HIP events on the layer's stream
+    # bracket only the dominant kernel's launches
+    hb.hb_set_kernel_timing(dl.layer, [dom])
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(a.steps):
         dl.run(reqs, x, hb.HB_OUT_F32, y)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ktimes = hb.hb_kernel_times(dl.layer, reset=True)
+    dom_ms, dom_n = hb.hb_kernel_times(dl.layer, reset=True)[dom]
     hb.hb_set_kernel_timing(dl.layer, False)
     ms_per_step = wall * 1e3 / a.steps
     log(f"bench: {ms_per_step:.4f} ms/step")
 
-    # same iteration without per-kernel events, and with the Infinity Cache flushed before each
+    # same iteration without any events, and with the Infinity Cache flushed before each
     flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(a.steps)]
     for i in range(a.steps):
@@ -198,19 +249,8 @@ def main() -> int:
     plain_ms = (time.perf_counter() - t1) * 1e3 / a.steps
     del flush
 
-    work = kernel_work(shape, [(c, xx) for c, xx, _ in reqs])
-    kernels = {}
-    for name, (tot, n) in ktimes.items():
-        if n == 0:
-            continue
-        avg_ms = tot / n
-        fl, by = work.get(name, (0.0, 0.0))
-        kernels[name] = {"avg_ms": round(avg_ms, 5), "launches": n,
-                         "tflops": round(fl / (avg_ms * 1e-3) / 1e12, 2) if fl else None,
-                         "gbps": round(by / (avg_ms * 1e-3) / 1e9, 1) if by else None}
-    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
     fl, by = work[dom]
-    avg_s = kernels[dom]["avg_ms"] * 1e-3
+    avg_s = dom_ms / dom_n * 1e-3
     if fl / by > RIDGE:
         roof = {"bound": "mfma", "achieved": round(fl / avg_s / 1e12, 2), "peak": PEAK_BF16 / 1e12,
                 "unit": "TFLOP/s"}
@@ -218,6 +258,8 @@ def main() -> int:
         roof = {"bound": "hbm", "achieved": round(by / avg_s / 1e9, 1), "peak": PEAK_HBM / 1e9, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     roof["kernel"] = dom
+    roof["avg_ms"] = round(dom_ms / dom_n, 5)
+    roof["launches_timed"] = dom_n
     roof["algorithmic_flops"] = fl
     roof["algorithmic_bytes"] = by
     tr = measured_traffic(dom, "llama3-8b")
@@ -266,7 +308,7 @@ def main() -> int:
                    "kv_heads": shape.n_kv_heads, "head_dim": shape.head_dim, "ffn": shape.ffn_dim,
                    "kv_block": 16, "parallelism": "none (1 GPU)"},
         "latency_ms": {"timed_region_per_step": round(ms_per_step, 5),
-                       "no_kernel_events": round(plain_ms, 5),
+                       "no_events": round(plain_ms, 5),
                        "cache_flushed_median": round(cold[len(cold) // 2], 5),
                        "cache_flushed_p10": round(cold[len(cold) // 10], 5),
                        "cache_flushed_p90": round(cold[(9 * len(cold)) // 10], 5)},
@@ -276,6 +318,7 @@ def main() -> int:
                            "roofline_time_us": round(max(flops / PEAK_BF16, bytes_ / PEAK_HBM) * 1e6, 1)},
         "roofline": roof,
         "kernels": kernels,
+        "kernels_note": "per-kernel averages from a separate pass with every launch bracketed by events",
         "cpu_baseline": cpu,
         "latency_profile": profile,
     }

@@ -187,16 +187,19 @@ hb_status hb_profile(hb_layer* layer, const int32_t* chunk_sizes, int32_t n_chun
                      const hb_decode_mix* mixes, int32_t n_mix, int32_t warmup, int32_t iters,
                      uint64_t seed, hb_profile_cell* out);
 
-/* Per-kernel timing of hb_run_iteration, for roofline accounting. While
- * enabled, every launch of an iteration is bracketed by HIP events on the
- * layer's stream. hb_kernel_times synchronises the stream and adds the elapsed
- * time (ms) and launch count of each kernel since the last reset into
- * total_ms[HB_K_COUNT] / launches[HB_K_COUNT]; reset != 0 starts a new tally. */
+/* Per-kernel timing of hb_run_iteration, for roofline accounting. Every
+ * launch of kernel k with bit k of kernel_mask set is bracketed by HIP events
+ * on the layer's stream (mask 0 turns timing off; timing one kernel keeps the
+ * event overhead off the others). hb_kernel_times synchronises the stream and
+ * adds the elapsed time (ms) and launch count of each kernel since the last
+ * reset into total_ms[HB_K_COUNT] / launches[HB_K_COUNT]; reset != 0 starts a
+ * new tally. Errors: HB_ERR_INVALID (null layer, mask bits beyond
+ * HB_K_COUNT), HB_ERR_HIP. */
 enum {
   HB_K_RMSNORM_ATTN = 0, HB_K_GEMM_QKV, HB_K_ROPE_KV, HB_K_ATTENTION, HB_K_ATTN_MERGE,
   HB_K_GEMM_O, HB_K_RMSNORM_FFN, HB_K_GEMM_GATE_UP, HB_K_GEMM_DOWN, HB_K_COUNT
 };
-hb_status hb_set_kernel_timing(hb_layer* layer, int32_t enable);
+hb_status hb_set_kernel_timing(hb_layer* layer, uint32_t kernel_mask);
 hb_status hb_kernel_times(hb_layer* layer, double* total_ms, int64_t* launches, int32_t reset);
 const char* hb_kernel_name(int32_t kernel);
 

@@ -64,7 +64,7 @@ struct hb_layer {
   Plan plan;
   int last_T = 0;
   // timing
-  bool timing = false;
+  uint32_t timing_mask = 0;  // bit k: bracket kernel k with events
   std::vector<hipEvent_t> ev_free;
   std::vector<TimedLaunch> timed;
   double tot_ms[HB_K_COUNT] = {};
@@ -165,7 +165,7 @@ hb_status get_event(hb_layer* L, hipEvent_t* e) {
 // Launch wrapper: brackets the launch with events while timing is enabled.
 template <typename F>
 hb_status timed(hb_layer* L, int kernel, F&& launch) {
-  if (!L->timing) {
+  if (!((L->timing_mask >> kernel) & 1u)) {
     launch();
     return HB_OK;
   }
@@ -410,9 +410,10 @@ hb_status hb_run_iteration(hb_layer* L, const hb_batch_desc* desc) {
   return enqueue_layer(L, desc);
 }
 
-hb_status hb_set_kernel_timing(hb_layer* L, int32_t enable) {
+hb_status hb_set_kernel_timing(hb_layer* L, uint32_t mask) {
   if (!L) return fail(HB_ERR_INVALID, "null layer");
-  L->timing = enable != 0;
+  if (mask >> HB_K_COUNT) return fail(HB_ERR_INVALID, "timing mask 0x%x has bits beyond the %d kernels", mask, HB_K_COUNT);
+  L->timing_mask = mask;
   return HB_OK;
 }
 

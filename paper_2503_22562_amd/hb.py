@@ -93,7 +93,7 @@ def load() -> C.CDLL:
     lib.hb_profile.argtypes = [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.POINTER(hb_decode_mix), C.c_int32,
                                C.c_int32, C.c_int32, C.c_uint64, C.POINTER(hb_profile_cell)]
     lib.hb_profile.restype = st
-    lib.hb_set_kernel_timing.argtypes = [C.c_void_p, C.c_int32]
+    lib.hb_set_kernel_timing.argtypes = [C.c_void_p, C.c_uint32]
     lib.hb_set_kernel_timing.restype = st
     lib.hb_kernel_times.argtypes = [C.c_void_p, C.POINTER(C.c_double), C.POINTER(C.c_int64), C.c_int32]
     lib.hb_kernel_times.restype = st
@@ -218,8 +218,18 @@ def hb_profile(layer: Layer, chunk_sizes: Sequence[int], mixes: Sequence[Tuple[S
     return res
 
 
-def hb_set_kernel_timing(layer: Layer, enable: bool) -> None:
-    _check(load().hb_set_kernel_timing(layer.handle, 1 if enable else 0))
+def hb_set_kernel_timing(layer: Layer, kernels) -> None:
+    """kernels: True (all), False (none) or an iterable of kernel names."""
+    if kernels is True:
+        mask = (1 << HB_K_COUNT) - 1
+    elif kernels is False or kernels is None:
+        mask = 0
+    else:
+        names = [hb_kernel_name(k) for k in range(HB_K_COUNT)]
+        mask = 0
+        for n in kernels:
+            mask |= 1 << names.index(n)
+    _check(load().hb_set_kernel_timing(layer.handle, mask))
 
 
 def hb_kernel_times(layer: Layer, reset: bool = False) -> Dict[str, Tuple[float, int]]:
