@@ -25,6 +25,9 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", f"-I{os.path.join(ROOT, 'include')}", f"
 # Packed fp32 instructions are kept out of the device code.
 HIP_FLAGS = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-ffp-contract=fast", "-munsafe-fp-atomics"]
+# The GEMM keeps its accumulators in ordinary VGPRs (MFMA with VGPR C/D
+# operands), which avoids accumulator copies between the two K halves.
+EXTRA_FLAGS = {"k_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def _compile(src: str) -> str:
@@ -33,7 +36,7 @@ def _compile(src: str) -> str:
     if src.endswith(".cpp"):
         cmd = ["g++", *COMMON, "-Wall", "-c", path, "-o", obj]
     else:
-        cmd = [HIPCC, *COMMON, *HIP_FLAGS, "-c", path, "-o", obj]
+        cmd = [HIPCC, *COMMON, *HIP_FLAGS, *EXTRA_FLAGS.get(src, []), "-c", path, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

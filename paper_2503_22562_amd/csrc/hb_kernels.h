@@ -32,6 +32,8 @@ struct GemmPlan {
 // force_cfg >= 0 / force_ksplit > 0 restrict the choice to one tile shape /
 // one K split where that split applies (testing).
 GemmPlan plan_gemm(const GemmArgs& a, int cu_count, int force_cfg = -1, int force_ksplit = 0);
+// Number of LDS-pipelined tile shapes (valid force_cfg values are 0..count-1).
+int gemm_tile_count();
 // `partial` holds ksplit * M * N fp32 when plan.ksplit > 1.
 void launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& plan, float* partial);
 

@@ -97,8 +97,8 @@ __device__ __forceinline__ void store_column(const AttnArgs& a, const AttnItem& 
                                              float m, float l, int grp) {
   const int G = a.nq / a.nkv;
   const int pi = c / G;
+  if (pi >= it.npos) return;  // column past the item's last position
   if (it.part < 0) {
-    if (pi >= it.npos) return;
     const int h = it.kv_head * G + (c - pi * G);
     const float inv = 1.0f / l;
     uint16_t* orow = a.o + (size_t)(it.tok0 + pi) * a.nq * HD + h * HD + 4 * grp;

@@ -70,13 +70,15 @@ void launch_rmsnorm(hipStream_t s, const void* x, bool x_f32, const uint16_t* g,
 
 // ---------------------------------------------------------------------------
 // RoPE + KV scatter: one workgroup per token. Angles p * theta^(-2j/hd) are
-// formed and evaluated in fp64, then rounded to fp32 for the rotation.
-// K goes to k_pool[blk][g][slot][d], V to v_pool[blk][g][slot/4][d][slot%4].
+// formed and evaluated in fp64, then rounded to fp32 for the rotation. A work
+// item rotates 8 dimension pairs (j, j + hd/2) of one q or k head with 16-byte
+// loads and stores. K goes to k_pool[blk][g][slot][d], V to
+// v_pool[blk][g][slot/4][d][slot%4].
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
   __shared__ float cs[64], sn[64];
   const int t = blockIdx.x, tid = threadIdx.x;
-  const int hd = a.hd, half = hd >> 1;
+  const int hd = a.hd, half = hd >> 1, hv = half >> 3;
   const int p = a.tok_pos[t];
   if (tid < half) {
     double sv, cv;
@@ -84,32 +86,39 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
     cs[tid] = (float)cv;
     sn[tid] = (float)sv;
   }
-  __syncthreads();
-  const uint16_t* row = a.qkv + (size_t)t * (a.nq + 2 * a.nkv) * hd;
-  // queries
-  for (int idx = tid; idx < a.nq * half; idx += 256) {
-    const int h = idx / half, j = idx - h * half;
-    const float u = bf16_to_f32(row[h * hd + j]), w = bf16_to_f32(row[h * hd + j + half]);
-    uint16_t* qo = a.q_out + (size_t)t * a.nq * hd + h * hd;
-    qo[j] = (uint16_t)f32_to_bf16(u * cs[j] - w * sn[j]);
-    qo[j + half] = (uint16_t)f32_to_bf16(w * cs[j] + u * sn[j]);
-  }
   const int blk = a.bt[a.req_bt[a.tok_req[t]] + (p >> 4)];
   const int slot = p & 15;
-  // keys (rotated) -> k_pool
-  const uint16_t* krow = row + a.nq * hd;
-  for (int idx = tid; idx < a.nkv * half; idx += 256) {
-    const int g = idx / half, j = idx - g * half;
-    const float u = bf16_to_f32(krow[g * hd + j]), w = bf16_to_f32(krow[g * hd + j + half]);
-    uint16_t* ko = a.k_pool + (((size_t)blk * a.nkv + g) * 16 + slot) * hd;
-    ko[j] = (uint16_t)f32_to_bf16(u * cs[j] - w * sn[j]);
-    ko[j + half] = (uint16_t)f32_to_bf16(w * cs[j] + u * sn[j]);
+  __syncthreads();
+  const uint16_t* row = a.qkv + (size_t)t * (a.nq + 2 * a.nkv) * hd;
+  // q heads 0..nq-1, then k heads (the row holds them contiguously)
+  for (int idx = tid; idx < (a.nq + a.nkv) * hv; idx += 256) {
+    const int h = idx / hv, j0 = 8 * (idx - h * hv);
+    const u32x4 lo = ld16(row + h * hd + j0), hi = ld16(row + h * hd + half + j0);
+    u32x4 r0, r1;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int j = j0 + 2 * e;
+      const float u0 = bf16_lo(lo[e]), u1 = bf16_hi(lo[e]), w0 = bf16_lo(hi[e]), w1 = bf16_hi(hi[e]);
+      r0[e] = pack_bf16x2(u0 * cs[j] - w0 * sn[j], u1 * cs[j + 1] - w1 * sn[j + 1]);
+      r1[e] = pack_bf16x2(w0 * cs[j] + u0 * sn[j], w1 * cs[j + 1] + u1 * sn[j + 1]);
+    }
+    uint16_t* dst = (h < a.nq) ? a.q_out + ((size_t)t * a.nq + h) * hd
+                               : a.k_pool + (((size_t)blk * a.nkv + (h - a.nq)) * 16 + slot) * hd;
+    st16(dst + j0, r0);
+    st16(dst + half + j0, r1);
   }
-  // values -> v_pool (dim-major inside the block)
-  const uint16_t* vrow = krow + a.nkv * hd;
-  for (int idx = tid; idx < a.nkv * hd; idx += 256) {
-    const int g = idx / hd, d = idx - g * hd;
-    a.v_pool[((size_t)blk * a.nkv + g) * 16 * hd + ((slot >> 2) * hd + d) * 4 + (slot & 3)] = vrow[idx];
+  // values -> v_pool (dim-major inside each group of four slots)
+  const uint16_t* vrow = row + (a.nq + a.nkv) * hd;
+  const int dv = hd >> 3;
+  for (int idx = tid; idx < a.nkv * dv; idx += 256) {
+    const int g = idx / dv, d0 = 8 * (idx - g * dv);
+    const u32x4 v = ld16(vrow + g * hd + d0);
+    uint16_t* dst = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * hd + ((slot >> 2) * hd + d0) * 4 + (slot & 3);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      dst[8 * e] = (uint16_t)(v[e] & 0xFFFFu);
+      dst[8 * e + 4] = (uint16_t)(v[e] >> 16);
+    }
   }
 }
 

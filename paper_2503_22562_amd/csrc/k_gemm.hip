@@ -162,16 +162,23 @@ static void launch_gemm_regstaged(hipStream_t s, const GemmArgs& a) {
 // ---------------------------------------------------------------------------
 // LDS-pipelined GEMM for K % 64 == 0.
 //
-// The K loop runs over a ring of STAGES LDS buffers that global memory fills
-// directly (16-byte global-to-LDS loads, no register staging), so up to
-// STAGES-1 K steps are in flight while one is multiplied. A 1-KB load
-// instruction of a wave fills eight 128-byte rows of a tile; inside a row the
-// eight 16-byte chunks are XOR-swizzled with the row index, so that the MFMA
-// fragment reads of eight consecutive rows fall into eight different chunk
-// positions. 4 waves in a 2 x 2 arrangement each own a (BM/2) x (BN/2) block
-// of 16x16 MFMA tiles. Workgroups are numbered so that the ones sharing a
-// weight tile run on the same XCD (one L2), and K can be split over several
-// workgroups whose fp32 partials a second kernel sums in a fixed order.
+// Tile BM x BN = 32 TM x 32 TN; 4 waves in a 2 x 2 arrangement each own a
+// 16 TM x 16 TN block of 16x16 MFMA tiles (accumulators in AGPRs). K advances
+// in stages of 64 through a ring of S LDS buffers that global memory fills
+// directly (16-byte global-to-LDS loads, no register staging). A 1-KB load
+// instruction of a wave fills eight 128-byte rows; inside a row the eight
+// 16-byte chunks are XOR-swizzled with the row index, so the fragment reads
+// of eight consecutive rows fall into eight different chunk positions.
+//
+// Software pipeline: a stage is consumed in two K halves of 32 whose MFMA
+// operands live in two register sets. While the MFMAs of one half run, the
+// fragment reads of the next half are issued between them (the scheduler is
+// told the interleave), so LDS latency and bandwidth hide under the matrix
+// cores. One barrier per stage, between the halves: after it, the buffer just
+// read is refilled with the stage S ahead and the next stage's first half is
+// read. Workgroups are numbered so that those sharing a weight tile run on the
+// same XCD (one L2); K can be split over workgroups whose fp32 partials a
+// second kernel sums in a fixed order.
 // ---------------------------------------------------------------------------
 namespace gemm_detail {
 
@@ -180,31 +187,77 @@ __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
+__device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-// One K step (64 columns) of the A and B tiles: each wave issues A_LOADS +
-// B_LOADS 1-KB global-to-LDS loads; lane L of a load lands at byte 16 L.
-template <int A_LOADS, int B_LOADS>
+// One K stage (64 columns) of the A and B tiles: LA (LB) 1-KB loads fill the
+// A (B) tile, 8 rows each; wave w issues loads w, w + NW, w + 2 NW, ...
+// (NA / NB slots, the last possibly empty); lane L of a load lands at byte 16 L.
+template <int NW, int LA, int LB>
 __device__ __forceinline__ void issue_stage(uint8_t* base, int a_bytes, const uint16_t* Abase, const uint16_t* Bbase,
                                             const uint32_t* aoff, const uint32_t* boff, int wave, int koff) {
+  constexpr int NA = (LA + NW - 1) / NW, NB = (LB + NW - 1) / NW;
 #pragma unroll
-  for (int j = 0; j < A_LOADS; ++j)
-    __builtin_amdgcn_global_load_lds(Abase + aoff[j] + koff, base + (wave * A_LOADS + j) * 1024, 16, 0, 0);
+  for (int j = 0; j < NA; ++j)
+    if (LA % NW == 0 || j * NW + wave < LA)
+      __builtin_amdgcn_global_load_lds(Abase + aoff[j] + koff, base + (j * NW + wave) * 1024, 16, 0, 0);
 #pragma unroll
-  for (int j = 0; j < B_LOADS; ++j)
-    __builtin_amdgcn_global_load_lds(Bbase + boff[j] + koff, base + a_bytes + (wave * B_LOADS + j) * 1024, 16, 0, 0);
+  for (int j = 0; j < NB; ++j)
+    if (LB % NW == 0 || j * NW + wave < LB)
+      __builtin_amdgcn_global_load_lds(Bbase + boff[j] + koff, base + a_bytes + (j * NW + wave) * 1024, 16, 0, 0);
 }
 
-template <int BM, int BN, int STAGES, int EPI>
-__global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a, int tiles_m, int tiles_n, int ksplit,
-                                                           int kchunk, float* __restrict__ partial) {
-  constexpr int WM = BM / 2, WN = BN / 2;
-  constexpr int TM = WM / 16, TN = WN / 16;
+// Fragment reads of one K half: TM A fragments (16-row blocks 2 KB apart)
+// and TN B fragments at the given per-fragment row offsets.
+template <int TM, int TN>
+__device__ __forceinline__ void read_frags(bf16x8 (&fa)[TM], bf16x8 (&fb)[TN], const uint8_t* ap, const uint8_t* bp,
+                                           const int (&broff)[TN]) {
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi) fa[mi] = as_bf16x8(*reinterpret_cast<const u32x4*>(ap + mi * 2048));
+#pragma unroll
+  for (int ni = 0; ni < TN; ++ni) fb[ni] = as_bf16x8(*reinterpret_cast<const u32x4*>(bp + broff[ni]));
+}
+
+template <int TM, int TN>
+__device__ __forceinline__ void mfma_block(f32x4 (&acc)[TM][TN], const bf16x8 (&fa)[TM], const bf16x8 (&fb)[TN]) {
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16x16x32(fb[ni], fa[mi], acc[mi][ni]);
+}
+
+// Scheduling directive for the region just emitted: NMFMA MFMAs with NREAD
+// LDS reads spread evenly between them, an MFMA first (its operands were read
+// one K half earlier, so the new reads never delay it).
+template <int NREAD, int NMFMA>
+__device__ __forceinline__ void interleave_reads() {
+  constexpr int per = NMFMA / NREAD > 0 ? NMFMA / NREAD : 1;
+  constexpr int groups = NMFMA / per < NREAD ? NMFMA / per : NREAD;
+  constexpr int extra = NMFMA - per * groups;
+#pragma unroll
+  for (int i = 0; i + 1 < groups; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, per, 0);  // `per` MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // then one LDS read
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, per, 0);
+  __builtin_amdgcn_sched_group_barrier(0x100, NREAD - groups + 1, 0);
+  if (extra > 0) __builtin_amdgcn_sched_group_barrier(0x008, extra, 0);
+}
+
+template <int TM, int TN, int WR, int WC, int S, int EPI>
+__global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int tiles_m, int tiles_n, int ksplit,
+                                                                  int kchunk, float* __restrict__ partial) {
+  constexpr int NW = WR * WC;
+  constexpr int WM = 16 * TM, WN = 16 * TN, BM = WM * WR, BN = WN * WC;
   constexpr int A_BYTES = BM * 128, STAGE_BYTES = (BM + BN) * 128;
-  constexpr int A_LOADS = BM / 32, B_LOADS = BN / 32, LOADS = A_LOADS + B_LOADS;
+  constexpr int LA = BM / 8, LB = BN / 8;                      // 1-KB loads per stage
+  constexpr int NA = (LA + NW - 1) / NW, NB = (LB + NW - 1) / NW;  // load slots per wave
+  constexpr int LOADS = LA / NW + LB / NW;                     // fewest loads any wave issues
+  static_assert(S >= 2 && (S - 2) * LOADS < 64, "stage count");
+  static_assert(EPI != GEMM_SWIGLU || (TN % 2 == 0), "gate/up pairs");
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
-  const int wm = wave >> 1, wn = wave & 1;
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int wm = wave / WC, wn = wave % WC;
   // XCD-aware tile order: workgroup g runs on XCD g % 8; give each XCD a
   // contiguous run of tiles, M fastest, so tiles sharing weights share an L2.
   const int total = tiles_m * tiles_n * ksplit;
@@ -219,19 +272,19 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a, int tiles_
   const int k_end = min(a.K, k_begin + kchunk);
   const int nk = (k_end - k_begin) >> 6;
 
-  // per-lane source offsets (elements) of this wave's load instructions,
-  // rows clamped in range: rows past M or N only feed outputs never stored
+  // per-lane source offsets (elements) of this wave's load slots, rows
+  // clamped in range: rows past M or N only feed outputs never stored
   const int lrow = lane >> 3;
   const int lchunk = (lane & 7) ^ lrow;
-  uint32_t aoff[A_LOADS], boff[B_LOADS];
+  uint32_t aoff[NA], boff[NB];
 #pragma unroll
-  for (int j = 0; j < A_LOADS; ++j) {
-    const int row = 8 * (wave * A_LOADS + j) + lrow;
+  for (int j = 0; j < NA; ++j) {
+    const int row = min(8 * (j * NW + wave) + lrow, BM - 1);
     aoff[j] = (uint32_t)min(m0 + row, M - 1) * (uint32_t)a.lda + 8 * lchunk;
   }
 #pragma unroll
-  for (int j = 0; j < B_LOADS; ++j) {
-    const int row = 8 * (wave * B_LOADS + j) + lrow;
+  for (int j = 0; j < NB; ++j) {
+    const int row = min(8 * (j * NW + wave) + lrow, BN - 1);
     int brow;
     if (EPI == GEMM_SWIGLU) {
       const int c = min(nt * (BN / 2) + (row % (BN / 2)), N - 1);
@@ -252,51 +305,68 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a, int tiles_
 
   // Fragment rows of a wave differ by multiples of 8, so the chunk swizzle
   // (row & 7) is that of the lane's own row: every fragment address is one
-  // per-lane base plus a compile-time offset. k-half kc flips chunk bit 2.
+  // per-lane base plus a compile-time offset. K half kc flips chunk bit 2.
   const int fr = lane & 15, fg = lane >> 4;
   const int swz = ((fg ^ (fr & 7)) << 4);
   const int a_lane = (wm * WM + fr) * 128 + swz;
-  const int b_lane = (EPI == GEMM_SWIGLU ? wn * (BN / 4) : wn * WN) * 128 + fr * 128 + swz;
+  const int b_lane = A_BYTES + (EPI == GEMM_SWIGLU ? wn * (WN / 2) : wn * WN) * 128 + fr * 128 + swz;
+  int broff[TN];
+#pragma unroll
+  for (int ni = 0; ni < TN; ++ni)
+    broff[ni] = 128 * ((EPI == GEMM_SWIGLU) ? ((ni < TN / 2) ? 16 * ni : BN / 2 + 16 * (ni - TN / 2)) : 16 * ni);
+
+  bf16x8 fa0[TM], fb0[TN], fa1[TM], fb1[TN];
 
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) issue_stage<A_LOADS, B_LOADS>(smem + s * STAGE_BYTES, A_BYTES, Abase, Bbase, aoff, boff, wave, s * 64);
-  for (int kt = 0; kt < nk; ++kt) {
-    // loads of step kt are complete once at most the later steps' are pending
-    const int ahead = min(STAGES - 2, nk - 1 - kt);
-    if (STAGES >= 4 && ahead >= 2) wait_vmcnt<(STAGES >= 4 ? 2 * LOADS : 0)>();
-    else if (STAGES >= 3 && ahead >= 1) wait_vmcnt<(STAGES >= 3 ? LOADS : 0)>();
+  for (int s = 0; s < S; ++s)
+    if (s < nk) issue_stage<NW, LA, LB>(smem + s * STAGE_BYTES, A_BYTES, Abase, Bbase, aoff, boff, wave, s * 64);
+  // stage 0 complete: the later prologue stages may stay in flight
+  {
+    const int pend = min(S, nk) - 1;
+    if (S >= 4 && pend >= 3) wait_vmcnt<(S >= 4 ? 3 * LOADS : 0)>();
+    else if (S >= 3 && pend >= 2) wait_vmcnt<(S >= 3 ? 2 * LOADS : 0)>();
+    else if (pend >= 1) wait_vmcnt<LOADS>();
+    else wait_vmcnt<0>();
+  }
+  __builtin_amdgcn_s_barrier();
+  read_frags<TM, TN>(fa0, fb0, smem + a_lane, smem + b_lane, broff);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // (the last stage is peeled so that every loop body is one straight block
+  // in which reads and MFMAs can be interleaved)
+  for (int kt = 0; kt < nk - 1; ++kt) {
+    const int buf = kt % S;
+    const uint8_t* st = smem + buf * STAGE_BYTES;
+    // first K half: read the second half's fragments under the MFMAs
+    read_frags<TM, TN>(fa1, fb1, st + (a_lane ^ 64), st + (b_lane ^ 64), broff);
+    mfma_block<TM, TN>(acc, fa0, fb0);
+    interleave_reads<TM + TN, TM * TN>();
+    __builtin_amdgcn_sched_barrier(0);
+    // this buffer is fully read (second-half fragments are in registers);
+    // the next stage must be complete, the later ones may stay in flight
+    wait_lgkm0();
+    const int pend = min(nk - kt - 2, S - 2);
+    if (S >= 4 && pend >= 2) wait_vmcnt<(S >= 4 ? 2 * LOADS : 0)>();
+    else if (S >= 3 && pend >= 1) wait_vmcnt<(S >= 3 ? LOADS : 0)>();
     else wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
-    if (kt + STAGES - 1 < nk)
-      issue_stage<A_LOADS, B_LOADS>(smem + ((kt + STAGES - 1) % STAGES) * STAGE_BYTES, A_BYTES, Abase, Bbase, aoff, boff,
-                                    wave, (kt + STAGES - 1) * 64);
-    const uint8_t* As = smem + (kt % STAGES) * STAGE_BYTES;
-    const uint8_t* Bs = As + A_BYTES;
-    // all fragment reads of the step first, so LDS latency overlaps the MFMAs
-    // (the compiler then waits on partial counts instead of after every read)
-    bf16x8 af[2][TM], bfr[2][TN];
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc) {
-      const uint8_t* ap = As + (a_lane ^ (kc << 6));
-      const uint8_t* bp = Bs + (b_lane ^ (kc << 6));
-#pragma unroll
-      for (int mi = 0; mi < TM; ++mi) af[kc][mi] = as_bf16x8(*reinterpret_cast<const u32x4*>(ap + mi * 2048));
-#pragma unroll
-      for (int ni = 0; ni < TN; ++ni) {
-        const int roff = (EPI == GEMM_SWIGLU) ? ((ni < TN / 2) ? 16 * ni : BN / 2 + 16 * (ni - TN / 2)) : 16 * ni;
-        bfr[kc][ni] = as_bf16x8(*reinterpret_cast<const u32x4*>(bp + roff * 128));
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc) {
-#pragma unroll
-      for (int mi = 0; mi < TM; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16x16x32(bfr[kc][ni], af[kc][mi], acc[mi][ni]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    if (kt + S < nk)
+      issue_stage<NW, LA, LB>(smem + buf * STAGE_BYTES, A_BYTES, Abase, Bbase, aoff, boff, wave, (kt + S) * 64);
+    __builtin_amdgcn_sched_barrier(0);
+    // second K half: read the next stage's first half under the MFMAs
+    const uint8_t* nx = smem + ((kt + 1) % S) * STAGE_BYTES;
+    read_frags<TM, TN>(fa0, fb0, nx + a_lane, nx + b_lane, broff);
+    mfma_block<TM, TN>(acc, fa1, fb1);
+    interleave_reads<TM + TN, TM * TN>();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (nk > 0) {
+    const uint8_t* st = smem + ((nk - 1) % S) * STAGE_BYTES;
+    read_frags<TM, TN>(fa1, fb1, st + (a_lane ^ 64), st + (b_lane ^ 64), broff);
+    mfma_block<TM, TN>(acc, fa0, fb0);
+    interleave_reads<TM + TN, TM * TN>();
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_block<TM, TN>(acc, fa1, fb1);
   }
 
   // epilogue: acc[mi][ni][i] = C[m][n + i]
@@ -310,7 +380,7 @@ __global__ __launch_bounds__(256, 1) void gemm_lds_kernel(GemmArgs a, int tiles_
     if (EPI == GEMM_SWIGLU) {
 #pragma unroll
       for (int ni = 0; ni < TN / 2; ++ni) {
-        const int n = nt * (BN / 2) + wn * (BN / 4) + 16 * ni + cq;
+        const int n = nt * (BN / 2) + wn * (WN / 2) + 16 * ni + cq;
         if (n >= N) continue;
         const f32x4 gt = acc[mi][ni], up = acc[mi][ni + TN / 2];
         u32x2 o;
@@ -389,59 +459,87 @@ namespace {
 using namespace gemm_detail;
 
 struct TileCfg {
-  int bm, bn, stages;
-  float eff;  // relative MFMA efficiency of the tile shape
+  int tm, tn, wr, wc, stages;  // per-wave MFMA blocks, wave grid, LDS stages
+  float stage_us, fixed_us;    // measured cost of one 64-wide K stage per round, and per round
 };
+// Accumulators and both fragment sets stay within the 256 VGPRs of a wave.
+// 8-wave workgroups put two waves on each SIMD; 4-wave ones with LDS rings
+// of at most 80 KB run two workgroups per CU. The costs were fitted to
+// MI355X timings of the layer's four GEMMs over M = 384..2304.
 constexpr TileCfg kTiles[] = {
-    {256, 256, 2, 1.00f}, {256, 128, 3, 0.90f}, {128, 256, 3, 0.90f}, {128, 128, 4, 0.75f}, {64, 256, 3, 0.70f},
+    {8, 4, 2, 2, 3, 0.969f, 2.6f},  {4, 8, 2, 2, 3, 0.999f, 1.0f}, {4, 4, 2, 2, 2, 0.892f, 6.9f},
+    {6, 4, 2, 2, 2, 1.019f, 17.9f}, {3, 8, 2, 2, 3, 0.842f, 2.1f}, {9, 4, 2, 2, 3, 1.095f, 1.8f},
+    {2, 8, 2, 2, 3, 0.744f, 0.0f},  {8, 4, 2, 4, 2, 1.295f, 15.8f}, {6, 4, 2, 4, 2, 1.323f, 0.2f},
+    {4, 4, 2, 4, 3, 0.864f, 7.3f},
 };
+constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 
-template <int BM, int BN, int ST, int EPI>
+template <int TM, int TN, int WR, int WC, int ST, int EPI>
 void launch_tile(hipStream_t s, const GemmArgs& a, int tiles_m, int tiles_n, int ksplit, int kchunk, float* partial) {
-  constexpr int lds = ST * (BM + BN) * 128;
+  constexpr int lds = ST * 16 * (TM * WR + TN * WC) * 128;
+  static_assert(lds <= 160 * 1024, "LDS");
   static bool attr = false;
   if (!attr) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_lds_kernel<BM, BN, ST, EPI>),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_pipe_kernel<TM, TN, WR, WC, ST, EPI>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     attr = true;
   }
-  gemm_lds_kernel<BM, BN, ST, EPI><<<tiles_m * tiles_n * ksplit, 256, lds, s>>>(a, tiles_m, tiles_n, ksplit, kchunk,
-                                                                                  partial);
+  gemm_pipe_kernel<TM, TN, WR, WC, ST, EPI>
+      <<<tiles_m * tiles_n * ksplit, 64 * WR * WC, lds, s>>>(a, tiles_m, tiles_n, ksplit, kchunk, partial);
 }
 
 template <int EPI>
 void launch_cfg(int idx, hipStream_t s, const GemmArgs& a, int tm, int tn, int ks, int kchunk, float* part) {
   switch (idx) {
-    case 0: launch_tile<256, 256, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
-    case 1: launch_tile<256, 128, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
-    case 2: launch_tile<128, 256, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
-    case 3: launch_tile<128, 128, 4, EPI>(s, a, tm, tn, ks, kchunk, part); break;
-    default: launch_tile<64, 256, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 0: launch_tile<8, 4, 2, 2, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 1: launch_tile<4, 8, 2, 2, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 2: launch_tile<4, 4, 2, 2, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 3: launch_tile<6, 4, 2, 2, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 4: launch_tile<3, 8, 2, 2, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 5: launch_tile<9, 4, 2, 2, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 6: launch_tile<2, 8, 2, 2, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 7: launch_tile<8, 4, 2, 4, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 8: launch_tile<6, 4, 2, 4, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    default: launch_tile<4, 4, 2, 4, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
   }
 }
 }  // namespace
+
+int gemm_tile_count() { return kNumTiles; }
+
+// Cost model (microseconds): workgroups run in rounds of one (two, for small
+// LDS rings) per CU, each round costing its K stages at the tile's measured
+// rate; a K split adds the fp32 partials' round trip through HBM and the
+// reduce launch.
+static int tiles_per_cu(const TileCfg& c) {
+  const int lds = c.stages * 16 * (c.tm * c.wr + c.tn * c.wc) * 128;
+  return (c.wr * c.wc == 4 && 2 * lds <= 160 * 1024) ? 2 : 1;
+}
 
 GemmPlan plan_gemm(const GemmArgs& a, int cu_count, int force_cfg, int force_ksplit) {
   GemmPlan best{-1, 0, 0, 1, 0};
   if (a.K % 64 != 0) return best;
   double best_cost = 1e300;
   const int ksteps = a.K / 64;
-  for (int i = 0; i < (int)(sizeof(kTiles) / sizeof(kTiles[0])); ++i) {
+  for (int i = 0; i < kNumTiles; ++i) {
     if (force_cfg >= 0 && i != force_cfg) continue;
     const TileCfg& c = kTiles[i];
-    const int ncols = (a.epi == GEMM_SWIGLU) ? c.bn / 2 : c.bn;
-    const int tm = (a.M + c.bm - 1) / c.bm, tn = (a.N + ncols - 1) / ncols;
-    for (int ks = 1; ks <= 8; ks *= 2) {
+    const int bm = 16 * c.tm * c.wr, bn = 16 * c.tn * c.wc;
+    const int ncols = (a.epi == GEMM_SWIGLU) ? bn / 2 : bn;
+    const int tm = (a.M + bm - 1) / bm, tn = (a.N + ncols - 1) / ncols;
+    const int slots = std::max(1, cu_count) * tiles_per_cu(c);
+    for (int ks = 1; ks <= 8; ++ks) {
       if (ks > 1 && (a.epi == GEMM_SWIGLU || ksteps < 4 * ks)) break;
       if (force_ksplit > 0 && ks != force_ksplit && !(a.epi == GEMM_SWIGLU && ks == 1)) continue;
-      const int kchunk = ((ksteps + ks - 1) / ks) * 64;
+      const int kst = (ksteps + ks - 1) / ks;
+      if ((ks - 1) * kst >= ksteps) continue;  // every split gets at least one stage
       const int nwg = tm * tn * ks;
-      const int rounds = (nwg + cu_count - 1) / cu_count;
-      double cost = (double)rounds * c.bm * c.bn * kchunk / c.eff;
-      if (ks > 1) cost += (double)a.M * a.N * (ks + 2) * 4.0 / (8e12 / 2.5e15) / 2 / cu_count;  // reduce pass
+      const int rounds = (nwg + slots - 1) / slots;
+      double cost = rounds * (kst * c.stage_us + c.fixed_us);
+      if (ks > 1) cost += (double)a.M * a.N * 4.0 * (2 * ks + 1) / 5e6 + 3.0;
       if (cost < best_cost * 0.999) {
         best_cost = cost;
-        best = GemmPlan{i, tm, tn, ks, kchunk};
+        best = GemmPlan{i, tm, tn, ks, kst * 64};
       }
     }
   }
