@@ -49,7 +49,7 @@ hb_status check_config(const hb_layer_config* c, Dims* d) {
   d->blk = 16;
   d->G = G;
   d->P = 16 / G;
-  d->BQ = 256 / G;
+  d->BQ = kTileCols / G;
   d->qkv_n = (d->nq + 2 * d->nkv) * d->hd;
   d->theta = c->rope_theta;
   d->eps = c->rms_eps;
@@ -142,7 +142,7 @@ void iteration_work(const Dims& d, const hb_request* reqs, int n, double* flops,
 
 static int round_up(int64_t x, int m) { return (int)((x + m - 1) / m * m); }
 
-void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p) {
+void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p, const PlanOptions& opt) {
   const int R = desc->n_requests;
   const hb_request* rq = desc->requests;
   int T = 0, nbt = 0;
@@ -156,21 +156,23 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p)
   p->T = T;
   p->R = R;
 
-  // A chunk that fills at least half a 256-column tile goes to the workgroup
+  // A chunk that fills at least half a workgroup tile goes to the workgroup
   // path; decodes and short chunks become 16-column wave items.
-  auto is_tile = [&](int r) { return (int64_t)rq[r].chunk_len * d.G >= 128; };
+  auto is_tile = [&](int r) { return (int64_t)rq[r].chunk_len * d.G >= kTileCols / 2; };
   double tile_keys = 0, item_keys = 0;
   for (int r = 0; r < R; ++r) {
     const int c = rq[r].chunk_len, x = rq[r].context_len, w = is_tile(r) ? d.BQ : d.P;
     for (int i0 = 0; i0 < c; i0 += w) (is_tile(r) ? tile_keys : item_keys) += (double)d.nkv * (x + std::min(c, i0 + w));
   }
   // split lengths (multiples of 64 keys): about one round of tile workgroups
-  // (each split also writes 256 columns of fp32 partials) and about four
+  // (each split also writes kTileCols columns of fp32 partials) and about four
   // items per wave slot (8 per compute unit), so long decodes do not set the
   // finishing time
   const int cus = std::max(1, cu_count);
-  const int S_t = std::max(1024, round_up((int64_t)(tile_keys / (1.0 * cus)) + 1, 64));
-  const int S_i = std::max(256, round_up((int64_t)(item_keys / (32.0 * cus)) + 1, 64));
+  const int S_t = opt.split_tile > 0 ? round_up(opt.split_tile, 64)
+                                     : std::max(1024, round_up((int64_t)(tile_keys / (1.0 * cus)) + 1, 64));
+  const int S_i = opt.split_item > 0 ? round_up(opt.split_item, 64)
+                                     : std::max(256, round_up((int64_t)(item_keys / (32.0 * cus)) + 1, 64));
   p->split_tile = S_t;
   p->split_item = S_i;
 
@@ -180,7 +182,7 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p)
   for (int r = 0; r < R; ++r) {
     const int c = rq[r].chunk_len, x = rq[r].context_len;
     const bool tile = is_tile(r);
-    const int w = tile ? d.BQ : d.P, S = tile ? S_t : S_i, ncol = tile ? 256 : 16;
+    const int w = tile ? d.BQ : d.P, S = tile ? S_t : S_i, ncol = tile ? kTileCols : 16;
     std::vector<AttnItem>& out = tile ? tiles : items;
     for (int g = 0; g < d.nkv; ++g) {
       for (int i0 = 0; i0 < c; i0 += w) {
@@ -208,14 +210,24 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p)
   std::stable_sort(items.begin(), items.end(), [](const AttnItem& x, const AttnItem& y) {
     return (x.kv_end - x.kv_begin) > (y.kv_end - y.kv_begin);
   });
-  // work units: one per tile, one per kItemsPerUnit items, interleaved evenly
-  // so that compute-bound and bandwidth-bound workgroups share the GPU
+  // work units: one per tile, one per kItemsPerUnit items, in alternating
+  // runs of one unit per CU: workgroups are handed out round-robin over the
+  // CUs, two per CU, so a CU's first two workgroups are a compute-bound tile
+  // and a bandwidth-bound item group, which overlap well
   const int nt = (int)tiles.size(), ni_units = ((int)items.size() + kItemsPerUnit - 1) / kItemsPerUnit;
   std::vector<int32_t> units;
   units.reserve(nt + ni_units);
-  for (int a = 0, b = 0; a < nt || b < ni_units;) {
-    if (b >= ni_units || (a < nt && (int64_t)a * ni_units <= (int64_t)b * nt)) units.push_back(a++);
-    else units.push_back(-1 - b++);
+  const int run = opt.unit_block != 0 ? opt.unit_block : cus;
+  if (run > 0) {
+    for (int a = 0, b = 0; a < nt || b < ni_units;) {
+      for (int k = 0; k < run && a < nt; ++k) units.push_back(a++);
+      for (int k = 0; k < run && b < ni_units; ++k) units.push_back(-1 - b++);
+    }
+  } else {
+    for (int a = 0, b = 0; a < nt || b < ni_units;) {
+      if (b >= ni_units || (a < nt && (int64_t)a * ni_units <= (int64_t)b * nt)) units.push_back(a++);
+      else units.push_back(-1 - b++);
+    }
   }
   p->n_tiles = nt;
   p->n_items = (int)items.size();

@@ -22,7 +22,7 @@ struct Dims {
   int H = 0, nq = 0, nkv = 0, hd = 0, F = 0, blk = 16;
   int G = 0;      // q heads per kv head
   int P = 0;      // query positions of a 16-column wave item = 16 / G
-  int BQ = 0;     // query positions of a 256-column workgroup tile = 256 / G
+  int BQ = 0;     // query positions of a workgroup tile = kTileCols / G
   int qkv_n = 0;  // (nq + 2 nkv) * hd
   float theta = 0.f, eps = 0.f;
   int max_T = 0, max_R = 0;
@@ -32,7 +32,7 @@ hb_status check_config(const hb_layer_config* cfg, Dims* d);
 
 // Attention work over the key positions [kv_begin, kv_end) of one request
 // and kv head: a wave item covers 16 query columns (P positions x G heads), a
-// workgroup tile 256 columns (BQ positions x G heads). part < 0: the unit
+// workgroup tile kTileCols columns (BQ positions x G heads). part < 0: the unit
 // writes the normalised output; otherwise its columns' partial results go to
 // column slots part + c.
 struct AttnItem {
@@ -48,8 +48,10 @@ static_assert(sizeof(AttnItem) == 32 && sizeof(MergeGroup) == 32, "packed as 8 i
 // Each request's block ids are followed by kBtPad copies of its last id, so
 // the four ids of a 64-key step can be read as one vector even at the end.
 constexpr int kBtPad = 3;
-// Wave items are grouped kItemsPerUnit to a workgroup (one per wave).
-constexpr int kItemsPerUnit = 8;
+// Query columns of a workgroup tile (32 per wave), and wave items grouped to
+// a workgroup (one per wave): the attention workgroup has 4 waves.
+constexpr int kTileCols = 128;
+constexpr int kItemsPerUnit = 4;
 
 struct Plan {
   int T = 0, R = 0;
@@ -73,8 +75,16 @@ struct SlotMarks {
 // Validate `desc` against the layer shape and a pool of num_blocks blocks.
 hb_status check_batch(const Dims& d, int num_blocks, const hb_batch_desc* desc, SlotMarks* marks);
 
+// Fixed split lengths (keys, multiples of 64; 0 = chosen from the batch),
+// for tuning and tests.
+struct PlanOptions {
+  int split_tile = 0, split_item = 0;
+  int unit_block = 0;  // runs of tiles / item groups in the unit order (0: one per CU; < 0: fine interleave)
+};
+
 // Build the plan of a validated batch for a GPU with cu_count compute units.
-void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p);
+void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p,
+                const PlanOptions& opt = PlanOptions());
 
 // Algorithmic flops and HBM bytes of one iteration (what the method must
 // compute and move, not what an implementation happens to do).

@@ -48,6 +48,7 @@ struct hb_layer {
   int device = 0, cu_count = 0;
   int gemm_tile = -1;   // HB_GEMM_TILE at creation: force one GEMM tile shape (testing)
   int gemm_ksplit = 0;  // HB_GEMM_KSPLIT at creation: force one K split (testing)
+  PlanOptions plan_opt;  // HB_ATTN_SPLIT_TILE / HB_ATTN_SPLIT_ITEM at creation (tuning, testing)
   // workspace
   uint16_t *xn = nullptr, *qkv = nullptr, *q_rot = nullptr, *attn = nullptr, *mlp = nullptr;
   float* h2 = nullptr;
@@ -352,6 +353,9 @@ hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w,
   L->cu_count = prop.multiProcessorCount;
   if (const char* e = std::getenv("HB_GEMM_TILE")) L->gemm_tile = std::atoi(e);
   if (const char* e = std::getenv("HB_GEMM_KSPLIT")) L->gemm_ksplit = std::atoi(e);
+  if (const char* e = std::getenv("HB_ATTN_SPLIT_TILE")) L->plan_opt.split_tile = std::atoi(e);
+  if (const char* e = std::getenv("HB_ATTN_SPLIT_ITEM")) L->plan_opt.split_item = std::atoi(e);
+  if (const char* e = std::getenv("HB_ATTN_UNIT_BLOCK")) L->plan_opt.unit_block = std::atoi(e);
   const size_t T = d.max_T;
   struct Alloc { void** p; size_t bytes; } allocs[] = {
       {(void**)&L->xn, T * d.H * 2},         {(void**)&L->qkv, T * d.qkv_n * 2},
@@ -406,7 +410,7 @@ hb_status hb_run_iteration(hb_layer* L, const hb_batch_desc* desc) {
   hb_status st = check_batch(L->d, L->pool.num_blocks, desc, &L->marks);
   if (st != HB_OK) return st;
   if (desc->n_requests == 0) return HB_OK;
-  build_plan(L->d, desc, L->cu_count, &L->plan);
+  build_plan(L->d, desc, L->cu_count, &L->plan, L->plan_opt);
   return enqueue_layer(L, desc);
 }
 

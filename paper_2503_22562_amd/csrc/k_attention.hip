@@ -12,14 +12,15 @@
 // (position, q head) pair; the G = n_q / n_kv heads of a kv head sit in
 // adjacent columns so each K/V byte serves all of them.
 //
-// Two kinds of work share the launch, one per 512-thread workgroup (8 waves,
-// two per SIMD, so one wave's softmax arithmetic overlaps the other's MFMAs):
-//  * chunk tiles: 256 columns (8 waves x 32) of one request and kv head over a
+// Two kinds of work share the launch, one per 256-thread workgroup (4 waves;
+// two workgroups per CU, so a compute-bound tile and a bandwidth-bound item
+// group can run side by side on one CU):
+//  * chunk tiles: 128 columns (4 waves x 32) of one request and kv head over a
 //    key range; 32-key K/V steps (two pool blocks) are copied into a 4-stage
 //    LDS ring by global-to-LDS loads and every wave reads them from there
 //    (K rows XOR-swizzled in 16-byte chunks so fragment reads do not collide
 //    in banks). Compute-bound: 32 MFMAs per wave per step.
-//  * wave items: 16 columns (decodes, short chunks) per wave, eight per
+//  * wave items: 16 columns (decodes, short chunks) per wave, four per
 //    workgroup; each wave streams its K/V straight into registers, the next
 //    32-key step loading while the current one is multiplied. HBM-bound.
 // The planner interleaves the two kinds so compute- and bandwidth-bound
@@ -37,7 +38,8 @@ namespace attn_detail {
 
 constexpr float NEG_BIG = -1.0e30f;
 constexpr int WSTEP = 32;   // keys per wave-item step = 2 pool blocks
-constexpr int WAVES = 8;    // waves per workgroup (2 per SIMD)
+constexpr int WAVES = 4;    // waves per workgroup (one per SIMD; two workgroups per CU)
+static_assert(WAVES == kItemsPerUnit && 32 * WAVES == kTileCols, "planner geometry");
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -61,17 +63,14 @@ __device__ __forceinline__ bool softmax_step(const float (&sv)[N], float sc, flo
   float mx = sv[0];
 #pragma unroll
   for (int i = 1; i < N; ++i) mx = fmaxf(mx, sv[i]);
-  mx = wave_max_xor(mx, 16);
-  mx = wave_max_xor(mx, 32);
+  mx = rows_max(mx);
   const float ms = mx * sc;  // -inf when every key of the step is masked
   const bool rescale = __any(ms > m + RESCALE_SLACK);
-  alpha = 1.0f;
-  if (rescale) {
-    const float mn = fmaxf(m, ms);
-    alpha = exp2f(m - mn);
-    l *= alpha;
-    m = mn;
-  }
+  // branch-free, so the caller's MFMAs can be scheduled across it
+  const float mn = rescale ? fmaxf(m, ms) : m;
+  alpha = __builtin_amdgcn_exp2f(m - mn);  // 1 without a rescale; 0 from the initial -1e30
+  l *= alpha;
+  m = mn;
   float ps = 0.f;
 #pragma unroll
   for (int i = 0; i < N; ++i) {
@@ -251,8 +250,7 @@ __device__ __forceinline__ void wave_item(const AttnArgs& a, const AttnItem& it,
   } else {
     wave_compute(A, it.kv_begin + WSTEP * s, it, pos, grp, a.scale_log2, qf, o, m, l);
   }
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
+  l = rows_sum(l);
   store_column<HD>(a, it, col, o, m, l, grp);
 }
 
@@ -264,50 +262,196 @@ constexpr int TSTAGES = 4;   // LDS ring depth of the tile path
 
 template <int HD>
 struct TileGeom {
-  static constexpr int BLK = 16 * HD * 2;        // bytes of one block of one head
-  static constexpr int STAGE = 4 * BLK;          // 2 K blocks then 2 V blocks
+  static constexpr int BLK = 16 * HD * 2;        // bytes of one K block of one head
   static constexpr int ROW = HD * 2;             // bytes of one key row
   static constexpr int LOADS = BLK / 1024;       // 1-KB loads per block
   static constexpr int KEYS_PER_LOAD = 1024 / ROW;
   static constexpr int CHUNKS = ROW / 16;        // 16-byte chunks per key row
+  // A V block is four groups of four keys (HD * 8 bytes each). At HD 128 the
+  // groups sit 1152 bytes apart in LDS, so the two groups a half-wave reads
+  // together fall into different halves of the 64 banks.
+  static constexpr int VGS = HD == 128 ? HD * 8 + 128 : HD * 8;
+  static constexpr int VBLK = 4 * VGS;
+  static constexpr int V_LOAD_STRIDE = HD == 128 ? VGS : 1024;  // LDS distance of consecutive 1-KB V loads
+  static constexpr int STAGE = 2 * BLK + 2 * VBLK;  // 2 K blocks then 2 V blocks
+  // 16-byte chunk c of K row r is stored at chunk c ^ kswz(r): the 16 rows a
+  // fragment read touches then cover all bank positions
+  static constexpr __host__ __device__ int kswz(int r) { return HD == 128 ? (r & 15) : ((r >> 1) & 7); }
 };
 
 // One step is four blocks in the stage: K of the two pool blocks (rows
-// XOR-swizzled by 16-byte chunk), then their V (verbatim). Waves 2b and 2b+1
-// copy block b, each half of its 1-KB loads.
+// chunk-swizzled), then their V (groups spaced by VGS). Wave b copies stage
+// block b: the K (b = 0, 1) or V (b = 2, 3) of pool block b & 1.
 template <int HD>
 __device__ __forceinline__ void tile_issue(uint8_t* stage, const AttnArgs& a, int id, int g, int wave, int lane) {
   using TG = TileGeom<HD>;
-  constexpr int HALF = TG::LOADS / 2;
-  const int b = wave >> 1, i0 = (wave & 1) * HALF;
+  const int b = wave;
   const size_t blk_stride = (size_t)a.nkv * 16 * HD;
   const size_t off = (size_t)id * blk_stride + (size_t)g * 16 * HD;
-  uint8_t* dst = stage + b * TG::BLK;
   if (b < 2) {
+    uint8_t* dst = stage + b * TG::BLK;
     const uint16_t* K = a.k_pool + off;
     const int kk_lane = lane / TG::CHUNKS, pc = lane % TG::CHUNKS;
 #pragma unroll
-    for (int j = 0; j < HALF; ++j) {
-      const int i = i0 + j;
+    for (int i = 0; i < TG::LOADS; ++i) {
       const int kk = i * TG::KEYS_PER_LOAD + kk_lane;
-      __builtin_amdgcn_global_load_lds(K + kk * HD + 8 * (pc ^ (kk & 7)), dst + i * 1024, 16, 0, 0);
+      const uint16_t* src = K + kk * HD + 8 * (pc ^ TG::kswz(kk));
+      __builtin_amdgcn_global_load_lds(src, dst + i * 1024, 16, 0, 0);
     }
   } else {
+    uint8_t* dst = stage + 2 * TG::BLK + (b - 2) * TG::VBLK;
     const uint8_t* V = reinterpret_cast<const uint8_t*>(a.v_pool + off);
 #pragma unroll
-    for (int j = 0; j < HALF; ++j) {
-      const int i = i0 + j;
-      __builtin_amdgcn_global_load_lds(V + i * 1024 + lane * 16, dst + i * 1024, 16, 0, 0);
+    for (int i = 0; i < TG::LOADS; ++i) {
+      uint8_t* d = dst + i * TG::V_LOAD_STRIDE;
+      __builtin_amdgcn_global_load_lds(V + i * 1024 + lane * 16, d, 16, 0, 0);
     }
   }
+}
+
+// Fragments of one step from a stage: K^T rows of both pool blocks (swizzled
+// chunks), and the V^T fragments (keys 4 grp..+3 of both blocks).
+template <int HD>
+__device__ __forceinline__ void tile_read_k(bf16x8 (&kf)[2][HD / 32], const uint8_t* st, int k_lane, int grp, int col) {
+  using TG = TileGeom<HD>;
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int kc = 0; kc < HD / 32; ++kc)
+      kf[b][kc] = as_bf16x8(*reinterpret_cast<const u32x4*>(st + b * TG::BLK + k_lane + (((4 * kc + grp) ^ TG::kswz(col)) << 4)));
+}
+
+template <int HD>
+__device__ __forceinline__ void tile_read_v(u32x4 (&vf)[HD / 16], const uint8_t* st, int v_lane) {
+  using TG = TileGeom<HD>;
+  const uint8_t* vs = st + 2 * TG::BLK + v_lane;
+#pragma unroll
+  for (int dt = 0; dt < HD / 16; ++dt) {
+    const u32x2 va = *reinterpret_cast<const u32x2*>(vs + dt * 128);
+    const u32x2 vb = *reinterpret_cast<const u32x2*>(vs + TG::VBLK + dt * 128);
+    vf[dt] = u32x4{va[0], va[1], vb[0], vb[1]};
+  }
+}
+
+template <int HD, int CT>
+__device__ __forceinline__ void tile_scores(f32x4 (&sc)[CT][2], const bf16x8 (&kf)[2][HD / 32],
+                                            const bf16x8 (&qf)[CT][HD / 32]) {
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      sc[ct][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kc = 0; kc < HD / 32; ++kc) sc[ct][b] = mfma16x16x32(kf[b][kc], qf[ct][kc], sc[ct][b]);
+    }
+}
+
+// Online softmax of one step for the wave's CT column tiles, branch-free.
+// MASKED: keys past a column's position or past kv_end get no weight, and the
+// V lanes of keys past kv_end are cleared (unwritten slots may hold
+// non-finite bits, and 0 * NaN would poison the sum).
+template <int HD, int CT, bool MASKED>
+__device__ __forceinline__ bool tile_softmax(const f32x4 (&sc)[CT][2], bf16x8 (&pf)[CT], u32x4 (&vf)[HD / 16],
+                                             float (&m)[CT], float (&l)[CT], float (&alpha)[CT],
+                                             const int (&pos)[CT], int j0, int kv_end, int grp, float scale) {
+  if (MASKED) {
+    uint32_t vm[4];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int k0 = j0 + 16 * b + 4 * grp;
+      vm[2 * b] = (k0 < kv_end ? 0xFFFFu : 0u) | (k0 + 1 < kv_end ? 0xFFFF0000u : 0u);
+      vm[2 * b + 1] = (k0 + 2 < kv_end ? 0xFFFFu : 0u) | (k0 + 3 < kv_end ? 0xFFFF0000u : 0u);
+    }
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) vf[dt][e] &= vm[e];
+  }
+  bool rescale = false;
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct) {
+    float sv[8], p[8];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sv[4 * b + i] = sc[ct][b][i];
+    if (MASKED) {
+      const int lim = min(pos[ct], kv_end - 1);
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (j0 + 16 * b + 4 * grp + i > lim) sv[4 * b + i] = -INFINITY;
+    }
+    rescale |= softmax_step<8>(sv, scale, m[ct], l[ct], alpha[ct], p);
+    pf[ct] = p_operand(p, 0);
+  }
+  return rescale;
+}
+
+template <int HD, int CT>
+__device__ __forceinline__ void tile_pv(f32x4 (&o)[CT][HD / 16], const u32x4 (&vf)[HD / 16], const bf16x8 (&pf)[CT]) {
+#pragma unroll
+  for (int dt = 0; dt < HD / 16; ++dt)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) o[ct][dt] = mfma16x16x32(as_bf16x8(vf[dt]), pf[ct], o[ct][dt]);
+}
+
+// One key step of a tile. The scores of this step (sc_cur) were formed one
+// step earlier; while their softmax runs on the vector ALUs, the next step's
+// scores go to the matrix cores (sc_next), so the two overlap within the wave.
+template <int HD, int CT, bool MASKED, bool LAST>
+__device__ __forceinline__ void tile_step(const AttnArgs& a, const AttnItem& it, uint8_t* smem, int kt, int nsteps,
+                                          const int32_t* btab, int kb0, int kb_last, int& next_id, int wave,
+                                          int lane, int k_lane, int v_lane, const bf16x8 (&qf)[CT][HD / 32],
+                                          const int (&pos)[CT], f32x4 (&o)[CT][HD / 16], float (&m)[CT],
+                                          float (&l)[CT], f32x4 (&sc_cur)[CT][2], f32x4 (&sc_next)[CT][2]) {
+  using TG = TileGeom<HD>;
+  const int grp = lane >> 4, col = lane & 15;
+  u32x4 vf[HD / 16];
+  tile_read_v<HD>(vf, smem + (kt % TSTAGES) * TG::STAGE, v_lane);
+  if (!LAST) {
+    // step kt + 1 complete (the one issued after it may stay in flight); the
+    // ring slot of step kt - 1 is free for step kt + TSTAGES - 1
+    if (kt + 2 < nsteps) wait_vmcnt<TG::LOADS>();
+    else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kt + TSTAGES - 1 < nsteps) {
+      tile_issue<HD>(smem + ((kt + TSTAGES - 1) % TSTAGES) * TG::STAGE, a, next_id, it.kv_head, wave, lane);
+      if (kt + TSTAGES < nsteps) next_id = const_load(btab + min(kb0 + 2 * (kt + TSTAGES) + (wave & 1), kb_last));
+    }
+    bf16x8 kf[2][HD / 32];
+    tile_read_k<HD>(kf, smem + ((kt + 1) % TSTAGES) * TG::STAGE, k_lane, grp, col);
+    tile_scores<HD, CT>(sc_next, kf, qf);
+  }
+  bf16x8 pf[CT];
+  float alpha[CT];
+  const bool rescale = tile_softmax<HD, CT, MASKED>(sc_cur, pf, vf, m, l, alpha, pos, it.kv_begin + TSTEP * kt,
+                                                    it.kv_end, grp, a.scale_log2);
+  // keep the weights' computation here, under the score MFMAs, rather than
+  // letting it sink past the rescale branch into the PV block
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct) {
+    u32x4 w = __builtin_bit_cast(u32x4, pf[ct]);
+    asm volatile("" : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]));
+    pf[ct] = __builtin_bit_cast(bf16x8, w);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if (rescale) {
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int dt = 0; dt < HD / 16; ++dt) o[ct][dt] *= alpha[ct];
+  }
+  tile_pv<HD, CT>(o, vf, pf);
 }
 
 template <int HD>
 __device__ __forceinline__ void tile_unit(const AttnArgs& a, const AttnItem& it, uint8_t* smem) {
   using TG = TileGeom<HD>;
   constexpr int KC = HD / 32, DT = HD / 16;
-  constexpr int CT = 2;  // 16-column tiles per wave (8 waves x 32 columns)
-  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
+  constexpr int CT = 2;  // 16-column tiles per wave (4 waves x 32 columns)
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int G = a.nq / a.nkv;
   const int col = lane & 15, grp = lane >> 4;
   const int g = it.kv_head;
@@ -331,9 +475,8 @@ __device__ __forceinline__ void tile_unit(const AttnArgs& a, const AttnItem& it,
   const int kb_last = (it.kv_end - 1) >> 4;
   const int kb0 = it.kv_begin >> 4;
   const int nsteps = (it.kv_end - it.kv_begin + TSTEP - 1) / TSTEP;
-  // pool block of step s copied by this wave (stage block wave/2 holds the K
-  // of pool block 0, 1 or the V of pool block 0, 1)
-  auto block_id = [&](int s) { return const_load(btab + min(kb0 + 2 * s + ((wave >> 1) & 1), kb_last)); };
+  // steps whose keys all lie below the tile's first position and kv_end need no mask
+  const int full = min(nsteps, max(0, (min(it.kv_end, it.pos0) - it.kv_begin) / TSTEP));
 
   f32x4 o[CT][DT];
 #pragma unroll
@@ -345,103 +488,53 @@ __device__ __forceinline__ void tile_unit(const AttnArgs& a, const AttnItem& it,
   for (int ct = 0; ct < CT; ++ct) { m[ct] = NEG_BIG; l[ct] = 0.f; }
 
   const int k_lane = col * TG::ROW;
-  const int v_lane = ((grp * HD + col) * 4) * 2;
-  int next_id = block_id(0);
+  const int v_lane = grp * TG::VGS + col * 8;
+  // prologue: steps 0..TSTAGES-2 in flight, scores of step 0
+  int next_id = const_load(btab + min(kb0 + (wave & 1), kb_last));
 #pragma unroll
   for (int s0 = 0; s0 < TSTAGES - 1; ++s0) {
     if (s0 < nsteps) tile_issue<HD>(smem + s0 * TG::STAGE, a, next_id, g, wave, lane);
-    if (s0 + 1 < nsteps) next_id = block_id(s0 + 1);
+    if (s0 + 1 < nsteps) next_id = const_load(btab + min(kb0 + 2 * (s0 + 1) + (wave & 1), kb_last));
   }
-  for (int kt = 0; kt < nsteps; ++kt) {
-    // this wave's loads of step kt are complete once at most those of the
-    // (up to TSTAGES - 2) later steps already issued are pending
-    const int ahead = min(TSTAGES - 2, nsteps - 1 - kt);
-    if (ahead >= 2) wait_vmcnt<2 * (TG::LOADS / 2)>();
-    else if (ahead == 1) wait_vmcnt<TG::LOADS / 2>();
-    else wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    const int j0 = it.kv_begin + TSTEP * kt;
-    uint8_t* st = smem + (kt % TSTAGES) * TG::STAGE;
-    if (j0 + TSTEP > it.kv_end) {
-      // clear V of keys past kv_end (unwritten slots may hold non-finite bits)
-      for (int e = tid; e < 2 * 16 * HD; e += 64 * WAVES) {
-        const int b = e / (16 * HD), r = e % (16 * HD), key = r / HD, d = r % HD;
-        if (j0 + 16 * b + key >= it.kv_end)
-          reinterpret_cast<uint16_t*>(st + 2 * TG::BLK + b * TG::BLK)[((key >> 2) * HD + d) * 4 + (key & 3)] = 0;
-      }
-      __syncthreads();
-    }
-    if (kt + TSTAGES - 1 < nsteps) {
-      tile_issue<HD>(smem + ((kt + TSTAGES - 1) % TSTAGES) * TG::STAGE, a, next_id, g, wave, lane);
-      if (kt + TSTAGES < nsteps) next_id = block_id(kt + TSTAGES);
-    }
-    // S^T = K Q^T: all K fragment reads first so LDS latency is paid once
+  if (nsteps >= 3) wait_vmcnt<2 * TG::LOADS>();
+  else if (nsteps == 2) wait_vmcnt<TG::LOADS>();
+  else wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  f32x4 sa[CT][2], sb[CT][2];
+  {
     bf16x8 kf[2][KC];
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int kc = 0; kc < KC; ++kc)
-        kf[b][kc] = as_bf16x8(*reinterpret_cast<const u32x4*>(st + b * TG::BLK + k_lane + (((4 * kc + grp) ^ (col & 7)) << 4)));
-    __builtin_amdgcn_sched_barrier(0);
-    f32x4 sc[CT][2];
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        sc[ct][b] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kc = 0; kc < KC; ++kc) sc[ct][b] = mfma16x16x32(kf[b][kc], qf[ct][kc], sc[ct][b]);
-      }
-    // V^T fragments (keys 4 grp..+3 of both blocks), read while the softmax runs
-    const uint8_t* vs = st + 2 * TG::BLK + v_lane;
-    bf16x8 vf[DT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const u32x2 va = *reinterpret_cast<const u32x2*>(vs + dt * 128);
-      const u32x2 vb = *reinterpret_cast<const u32x2*>(vs + TG::BLK + dt * 128);
-      vf[dt] = as_bf16x8(u32x4{va[0], va[1], vb[0], vb[1]});
-    }
-    const bool masked = (j0 + TSTEP > it.kv_end) || (j0 + TSTEP > it.pos0);  // wave-uniform
-    bf16x8 pf[CT];
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct) {
-      float sv[8], p[8];
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) sv[4 * b + i] = sc[ct][b][i];
-      if (masked) {
-        const int lim = min(pos[ct], it.kv_end - 1);
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (j0 + 16 * b + 4 * grp + i > lim) sv[4 * b + i] = -INFINITY;
-      }
-      float alpha;
-      if (softmax_step<8>(sv, a.scale_log2, m[ct], l[ct], alpha, p)) {
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[ct][dt] *= alpha;
-      }
-      pf[ct] = p_operand(p, 0);
-    }
-    // O^T += V^T P^T
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct) o[ct][dt] = mfma16x16x32(vf[dt], pf[ct], o[ct][dt]);
+    tile_read_k<HD>(kf, smem, k_lane, grp, col);
+    tile_scores<HD, CT>(sa, kf, qf);
+  }
+  // steps alternate the two score buffers; the last step is peeled
+  int kt = 0;
+  for (; kt + 2 <= full && kt + 2 < nsteps; kt += 2) {
+    tile_step<HD, CT, false, false>(a, it, smem, kt, nsteps, btab, kb0, kb_last, next_id, wave, lane, k_lane, v_lane,
+                                    qf, pos, o, m, l, sa, sb);
+    tile_step<HD, CT, false, false>(a, it, smem, kt + 1, nsteps, btab, kb0, kb_last, next_id, wave, lane, k_lane,
+                                    v_lane, qf, pos, o, m, l, sb, sa);
+  }
+  for (; kt + 2 < nsteps; kt += 2) {
+    tile_step<HD, CT, true, false>(a, it, smem, kt, nsteps, btab, kb0, kb_last, next_id, wave, lane, k_lane, v_lane,
+                                   qf, pos, o, m, l, sa, sb);
+    tile_step<HD, CT, true, false>(a, it, smem, kt + 1, nsteps, btab, kb0, kb_last, next_id, wave, lane, k_lane,
+                                   v_lane, qf, pos, o, m, l, sb, sa);
+  }
+  if (kt + 1 < nsteps) {
+    tile_step<HD, CT, true, false>(a, it, smem, kt, nsteps, btab, kb0, kb_last, next_id, wave, lane, k_lane, v_lane,
+                                   qf, pos, o, m, l, sa, sb);
+    tile_step<HD, CT, true, true>(a, it, smem, kt + 1, nsteps, btab, kb0, kb_last, next_id, wave, lane, k_lane, v_lane,
+                                  qf, pos, o, m, l, sb, sa);
+  } else {
+    tile_step<HD, CT, true, true>(a, it, smem, kt, nsteps, btab, kb0, kb_last, next_id, wave, lane, k_lane, v_lane,
+                                  qf, pos, o, m, l, sa, sb);
   }
 #pragma unroll
-  for (int ct = 0; ct < CT; ++ct) {
-    float lt = l[ct];
-    lt += __shfl_xor(lt, 16, 64);
-    lt += __shfl_xor(lt, 32, 64);
-    store_column<HD>(a, it, 32 * wave + 16 * ct + col, o[ct], m[ct], lt, grp);
-  }
+  for (int ct = 0; ct < CT; ++ct) store_column<HD>(a, it, 32 * wave + 16 * ct + col, o[ct], m[ct], rows_sum(l[ct]), grp);
 }
 
 template <int HD>
-__global__ __launch_bounds__(64 * WAVES, 1) void attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64 * WAVES, 2) void attn_kernel(AttnArgs a) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   const int unit = const_load(a.units + blockIdx.x);
   if (unit >= 0) {

@@ -29,6 +29,7 @@ int main() {
   hb::build_plan(d, &desc, cu, &p);
   const int32_t* m = p.meta.data();
   printf("T %d %d %d %d\n", p.T, p.split_tile, p.split_item, p.n_slots);
+  printf("geom %d %d\n", hb::kTileCols, hb::kItemsPerUnit);
   auto dump = [&](const char* tag, int off, int n) {
     for (int i = 0; i < n; ++i) {
       printf("%s", tag);

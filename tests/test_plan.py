@@ -53,7 +53,8 @@ def check(plan, shape, reqs):
     # coverage: (token, kv head) -> list of key ranges
     cover = defaultdict(list)
     slots = []
-    for kind, width in (("tile", 256), ("item", 16)):
+    tile_cols, per_unit = plan["geom"][0]
+    for kind, width in (("tile", tile_cols), ("item", 16)):
         for req, g, tok0, pos0, npos, kb, ke, part in plan[kind]:
             assert kb % 64 == 0 and kb < ke and npos * G <= width
             assert tok0 == starts[req] + pos0 - reqs[req][1]
@@ -80,15 +81,15 @@ def check(plan, shape, reqs):
     # merge groups and their 16-column merge units
     want = []
     for gi, (p0, n, stride, tok0, npos, g, _, _) in enumerate(plan["group"]):
-        assert n > 1 and stride in (16, 256) and npos * G <= stride
+        assert n > 1 and stride in (16, tile_cols) and npos * G <= stride
         want += [gi * 16 + cb for cb in range(-(-npos * G // 16))]
     assert sorted(u[0] for u in plan["merge"]) == want
-    # units: each tile once, each group of eight items once
+    # units: each tile once, each group of per_unit items once
     units = [u[0] for u in plan["unit"]]
     tiles = sorted(u for u in units if u >= 0)
     groups = sorted(-1 - u for u in units if u < 0)
     assert tiles == list(range(len(plan["tile"])))
-    assert groups == list(range(-(-len(plan["item"]) // 8)))
+    assert groups == list(range(-(-len(plan["item"]) // per_unit)))
 
 
 SHAPES = {"tiny": (256, 4, 2, 64, 688), "8b": (4096, 32, 8, 128, 14336), "70b": (8192, 64, 8, 128, 28672),
