@@ -76,6 +76,16 @@ __device__ __forceinline__ T const_load(const T* p) {
   return __builtin_bit_cast(T, b);
 }
 
+// Sum over all 64 lanes, on the vector ALUs: lane swaps within quads, within
+// 8- and 16-lane rows (DPP mirrors), then across rows.
+__device__ __forceinline__ float wave_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xF, 0xF, false));  // row_half_mirror
+  v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xF, 0xF, false));  // row_mirror
+  return rows_sum(v);
+}
+
 // Index of the calling wave in its workgroup, as a wave-uniform value (so
 // loads addressed by it become scalar loads).
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }

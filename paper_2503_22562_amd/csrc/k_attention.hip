@@ -321,15 +321,27 @@ __device__ __forceinline__ void tile_read_k(bf16x8 (&kf)[2][HD / 32], const uint
       kf[b][kc] = as_bf16x8(*reinterpret_cast<const u32x4*>(st + b * TG::BLK + k_lane + (((4 * kc + grp) ^ TG::kswz(col)) << 4)));
 }
 
-template <int HD>
-__device__ __forceinline__ void tile_read_v(u32x4 (&vf)[HD / 16], const uint8_t* st, int v_lane) {
+// MASKED: the V lanes of keys past kv_end are cleared (unwritten slots may
+// hold non-finite bits, and 0 * NaN would poison the sum).
+template <int HD, bool MASKED>
+__device__ __forceinline__ void tile_read_v(u32x4 (&vf)[HD / 16], const uint8_t* st, int v_lane, int j0, int kv_end,
+                                            int grp) {
   using TG = TileGeom<HD>;
   const uint8_t* vs = st + 2 * TG::BLK + v_lane;
+  uint32_t vm[4] = {~0u, ~0u, ~0u, ~0u};
+  if (MASKED) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int k0 = j0 + 16 * b + 4 * grp;
+      vm[2 * b] = (k0 < kv_end ? 0xFFFFu : 0u) | (k0 + 1 < kv_end ? 0xFFFF0000u : 0u);
+      vm[2 * b + 1] = (k0 + 2 < kv_end ? 0xFFFFu : 0u) | (k0 + 3 < kv_end ? 0xFFFF0000u : 0u);
+    }
+  }
 #pragma unroll
   for (int dt = 0; dt < HD / 16; ++dt) {
     const u32x2 va = *reinterpret_cast<const u32x2*>(vs + dt * 128);
     const u32x2 vb = *reinterpret_cast<const u32x2*>(vs + TG::VBLK + dt * 128);
-    vf[dt] = u32x4{va[0], va[1], vb[0], vb[1]};
+    vf[dt] = u32x4{va[0] & vm[0], va[1] & vm[1], vb[0] & vm[2], vb[1] & vm[3]};
   }
 }
 
@@ -347,26 +359,11 @@ __device__ __forceinline__ void tile_scores(f32x4 (&sc)[CT][2], const bf16x8 (&k
 }
 
 // Online softmax of one step for the wave's CT column tiles, branch-free.
-// MASKED: keys past a column's position or past kv_end get no weight, and the
-// V lanes of keys past kv_end are cleared (unwritten slots may hold
-// non-finite bits, and 0 * NaN would poison the sum).
+// MASKED: keys past a column's position or past kv_end get no weight.
 template <int HD, int CT, bool MASKED>
-__device__ __forceinline__ bool tile_softmax(const f32x4 (&sc)[CT][2], bf16x8 (&pf)[CT], u32x4 (&vf)[HD / 16],
-                                             float (&m)[CT], float (&l)[CT], float (&alpha)[CT],
-                                             const int (&pos)[CT], int j0, int kv_end, int grp, float scale) {
-  if (MASKED) {
-    uint32_t vm[4];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int k0 = j0 + 16 * b + 4 * grp;
-      vm[2 * b] = (k0 < kv_end ? 0xFFFFu : 0u) | (k0 + 1 < kv_end ? 0xFFFF0000u : 0u);
-      vm[2 * b + 1] = (k0 + 2 < kv_end ? 0xFFFFu : 0u) | (k0 + 3 < kv_end ? 0xFFFF0000u : 0u);
-    }
-#pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) vf[dt][e] &= vm[e];
-  }
+__device__ __forceinline__ bool tile_softmax(const f32x4 (&sc)[CT][2], bf16x8 (&pf)[CT], float (&m)[CT],
+                                             float (&l)[CT], float (&alpha)[CT], const int (&pos)[CT], int j0,
+                                             int kv_end, int grp, float scale) {
   bool rescale = false;
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct) {
@@ -408,8 +405,10 @@ __device__ __forceinline__ void tile_step(const AttnArgs& a, const AttnItem& it,
                                           float (&l)[CT], f32x4 (&sc_cur)[CT][2], f32x4 (&sc_next)[CT][2]) {
   using TG = TileGeom<HD>;
   const int grp = lane >> 4, col = lane & 15;
+  // V fragments of this step (their LDS latency hides under the score MFMAs)
+  const int j0 = it.kv_begin + TSTEP * kt;
   u32x4 vf[HD / 16];
-  tile_read_v<HD>(vf, smem + (kt % TSTAGES) * TG::STAGE, v_lane);
+  tile_read_v<HD, MASKED>(vf, smem + (kt % TSTAGES) * TG::STAGE, v_lane, j0, it.kv_end, grp);
   if (!LAST) {
     // step kt + 1 complete (the one issued after it may stay in flight); the
     // ring slot of step kt - 1 is free for step kt + TSTAGES - 1
@@ -426,8 +425,7 @@ __device__ __forceinline__ void tile_step(const AttnArgs& a, const AttnItem& it,
   }
   bf16x8 pf[CT];
   float alpha[CT];
-  const bool rescale = tile_softmax<HD, CT, MASKED>(sc_cur, pf, vf, m, l, alpha, pos, it.kv_begin + TSTEP * kt,
-                                                    it.kv_end, grp, a.scale_log2);
+  const bool rescale = tile_softmax<HD, CT, MASKED>(sc_cur, pf, m, l, alpha, pos, j0, it.kv_end, grp, a.scale_log2);
   // keep the weights' computation here, under the score MFMAs, rather than
   // letting it sink past the rescale branch into the PV block
 #pragma unroll
@@ -548,7 +546,8 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_kernel(AttnArgs a) {
 
 // Merge of split work: one workgroup per (merge group, 16 columns), one
 // thread per (column, 8 dims), folding the parts in order with the online
-// rule: M' = max(M, m_s), acc' = acc 2^(M-M') + O_s 2^(m_s-M'), likewise L.
+// rule: M' = max(M, m_s), acc' = acc 2^(M-M') + O_s 2^(m_s-M'), likewise L
+// (several parts per fold, all of their loads issued together).
 template <int HD>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   const int mu = const_load(a.merge_units + blockIdx.x);
@@ -559,18 +558,37 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   if (threadIdx.x >= 16 * TPC || c >= gr.npos * G) return;
   const int d = (threadIdx.x % TPC) * 8;
   float M = NEG_BIG, L = 0.f, acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < gr.nparts; ++s) {
-    const size_t slot = (size_t)gr.part0 + (size_t)s * gr.stride + c;
-    const u32x2 ml = ld8(a.part_ml + slot * 2);
-    const float ms = __uint_as_float(ml[0]), ls = __uint_as_float(ml[1]);
-    const u32x4 o0 = ld16(a.part_o + slot * HD + d), o1 = ld16(a.part_o + slot * HD + d + 4);
-    const float Mn = fmaxf(M, ms);
-    const float wa = exp2f(M - Mn), wb = exp2f(ms - Mn);
-    L = L * wa + ls * wb;
+  // parts are folded four at a time so their loads are in flight together
+  constexpr int B = 4;
+  for (int s0 = 0; s0 < gr.nparts; s0 += B) {
+    float ms[B], ls[B];
+    u32x4 o0[B], o1[B];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      acc[j] = acc[j] * wa + __uint_as_float(o0[j]) * wb;
-      acc[4 + j] = acc[4 + j] * wa + __uint_as_float(o1[j]) * wb;
+    for (int j = 0; j < B; ++j) {
+      const int s = min(s0 + j, gr.nparts - 1);
+      const size_t slot = (size_t)gr.part0 + (size_t)s * gr.stride + c;
+      const u32x2 ml = ld8(a.part_ml + slot * 2);
+      ms[j] = (s0 + j < gr.nparts) ? __uint_as_float(ml[0]) : NEG_BIG;
+      ls[j] = __uint_as_float(ml[1]);
+      o0[j] = ld16(a.part_o + slot * HD + d);
+      o1[j] = ld16(a.part_o + slot * HD + d + 4);
+    }
+    float Mn = M;
+#pragma unroll
+    for (int j = 0; j < B; ++j) Mn = fmaxf(Mn, ms[j]);
+    const float wa = exp2f(M - Mn);
+    L *= wa;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] *= wa;
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      const float wb = (s0 + j < gr.nparts) ? exp2f(ms[j] - Mn) : 0.f;
+      L += ls[j] * wb;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[e] += __uint_as_float(o0[j][e]) * wb;
+        acc[4 + e] += __uint_as_float(o1[j][e]) * wb;
+      }
     }
     M = Mn;
   }

@@ -34,8 +34,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const void* __restrict__ x
       for (int j = 0; j < 8; ++j) ss += v[i][j] * v[i][j];
     }
   }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+  ss = wave_sum(ss);
   if ((tid & 63) == 0) red[tid >> 6] = ss;
   __syncthreads();
   const float tot = red[0] + red[1] + red[2] + red[3];
@@ -70,7 +69,7 @@ void launch_rmsnorm(hipStream_t s, const void* x, bool x_f32, const uint16_t* g,
 
 // ---------------------------------------------------------------------------
 // RoPE + KV scatter: one workgroup per token. Angles p * theta^(-2j/hd) are
-// formed and evaluated in fp64, then rounded to fp32 for the rotation. A work
+// formed and reduced modulo 2 pi in fp64, then evaluated in fp32. A work
 // item rotates 8 dimension pairs (j, j + hd/2) of one q or k head with 16-byte
 // loads and stores. K goes to k_pool[blk][g][slot][d], V to
 // v_pool[blk][g][slot/4][d][slot%4].
@@ -81,10 +80,14 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
   const int hd = a.hd, half = hd >> 1, hv = half >> 3;
   const int p = a.tok_pos[t];
   if (tid < half) {
-    double sv, cv;
-    sincos((double)p * a.inv_freq[tid], &sv, &cv);
-    cs[tid] = (float)cv;
-    sn[tid] = (float)sv;
+    // angle formed and reduced to [-pi, pi] in fp64, then evaluated in fp32
+    // (the rotation itself is fp32, and its inputs and outputs bf16)
+    const double ang = (double)p * a.inv_freq[tid];
+    const double r = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
+    float sv, cv;
+    sincosf((float)r, &sv, &cv);
+    cs[tid] = cv;
+    sn[tid] = sv;
   }
   const int blk = a.bt[a.req_bt[a.tok_req[t]] + (p >> 4)];
   const int slot = p & 15;
