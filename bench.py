@@ -43,8 +43,8 @@ def kernel_work(shape, requests, out_f32=True):
     yb = 4 if out_f32 else 2
     return {
         "rmsnorm_attn": (4.0 * T * H, 2.0 * T * H + 2 * H + 2.0 * T * H),
+        # QKV projection with RoPE and the paged K/V scatter in its epilogue
         "gemm_qkv": (2.0 * T * H * qkv_n, 2.0 * (H * qkv_n + T * H + T * qkv_n)),
-        "rope_kv": (6.0 * T * (nq + nkv) * hd, 2.0 * T * qkv_n + 2.0 * T * qd + 2.0 * T * 2 * nkv * hd),
         "attention": (4.0 * nq * hd * pairs, 2.0 * 2 * nkv * hd * kv_tok + 2.0 * T * qd * 2),
         "gemm_o": (2.0 * T * qd * H, 2.0 * H * qd + 2.0 * T * qd + 2.0 * T * H + 4.0 * T * H),
         "rmsnorm_ffn": (4.0 * T * H, 4.0 * T * H + 2 * H + 2.0 * T * H),

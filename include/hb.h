@@ -196,7 +196,7 @@ hb_status hb_profile(hb_layer* layer, const int32_t* chunk_sizes, int32_t n_chun
  * new tally. Errors: HB_ERR_INVALID (null layer, mask bits beyond
  * HB_K_COUNT), HB_ERR_HIP. */
 enum {
-  HB_K_RMSNORM_ATTN = 0, HB_K_GEMM_QKV, HB_K_ROPE_KV, HB_K_ATTENTION, HB_K_ATTN_MERGE,
+  HB_K_RMSNORM_ATTN = 0, HB_K_GEMM_QKV, HB_K_ATTENTION, HB_K_ATTN_MERGE,
   HB_K_GEMM_O, HB_K_RMSNORM_FFN, HB_K_GEMM_GATE_UP, HB_K_GEMM_DOWN, HB_K_COUNT
 };
 hb_status hb_set_kernel_timing(hb_layer* layer, uint32_t kernel_mask);

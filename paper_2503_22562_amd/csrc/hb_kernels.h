@@ -6,16 +6,36 @@
 
 namespace hb {
 
-// out[t][:] = bf16( x[t][:] / sqrt(mean(x[t]^2) + eps) * g ), x bf16 or fp32.
-void launch_rmsnorm(hipStream_t s, const void* x, bool x_f32, const uint16_t* g, uint16_t* out, int T, int H,
-                    float eps);
+// Per-token RoPE inputs for the QKV epilogue, written by the first RMSNorm:
+// cs[t][0..hd/2) = cos, cs[t][hd/2..hd) = sin of the angles pos(t) * inv_freq
+// (formed and reduced mod 2 pi in fp64, evaluated in fp32), and slot[t] =
+// 16 * pool block + slot of the token's new K/V.
+struct RopePrep {
+  const int32_t* tok_pos;
+  const int32_t* tok_req;
+  const int32_t* req_bt;
+  const int32_t* bt;
+  const double* inv_freq;
+  int hd;
+  float* cs;
+  int32_t* slot;
+};
 
-enum GemmEpilogue { GEMM_STORE_BF16 = 0, GEMM_RESIDUAL = 1, GEMM_SWIGLU = 2 };
+// out[t][:] = bf16( x[t][:] / sqrt(mean(x[t]^2) + eps) * g ), x bf16 or fp32;
+// with rope, also the RoPE inputs of every token.
+void launch_rmsnorm(hipStream_t s, const void* x, bool x_f32, const uint16_t* g, uint16_t* out, int T, int H,
+                    float eps, const RopePrep* rope = nullptr);
+
+enum GemmEpilogue { GEMM_STORE_BF16 = 0, GEMM_RESIDUAL = 1, GEMM_SWIGLU = 2, GEMM_QKV_ROPE = 3 };
 
 // C[M][N] = A[M][K] * B[N][K]^T with an epilogue:
 //   GEMM_STORE_BF16: C bf16
 //   GEMM_RESIDUAL:   C = R + A B^T, R bf16 or fp32, C fp32 or bf16
 //   GEMM_SWIGLU:     B has 2N rows [gate | up]; C bf16 = silu(A Bg^T) * (A Bu^T)
+//   GEMM_QKV_ROPE:   the columns are [q heads | k heads | v heads] of head_dim
+//                    each; q and k are rotated (rotate-half RoPE with the
+//                    per-row cos/sin of rope_cs), q goes to C [M][nq*hd], k
+//                    and v to the paged pool slot tok_slot[m] (no K split)
 struct GemmArgs {
   const uint16_t* A; int lda;
   const uint16_t* B; int ldb;
@@ -23,6 +43,10 @@ struct GemmArgs {
   void* C; int ldc; int c_f32;
   const void* R; int ldr; int r_f32;
   int epi;
+  // GEMM_QKV_ROPE only
+  const float* rope_cs; const int32_t* tok_slot;
+  uint16_t* k_pool; uint16_t* v_pool;
+  int nq, nkv, hd;
 };
 // Tile shape, grid and K split chosen for one GEMM (cfg < 0: the
 // register-staged kernel, used when K is not a multiple of 64).
@@ -36,22 +60,6 @@ GemmPlan plan_gemm(const GemmArgs& a, int cu_count, int force_cfg = -1, int forc
 int gemm_tile_count();
 // `partial` holds ksplit * M * N fp32 when plan.ksplit > 1.
 void launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& plan, float* partial);
-
-// Rotate q and k of every batch token at its position and store k and v in the
-// paged pool; q goes to q_out [T][nq*hd].
-struct RopeKvArgs {
-  const uint16_t* qkv;  // [T][(nq + 2 nkv) hd]
-  int T, nq, nkv, hd;
-  const int32_t* tok_pos;
-  const int32_t* tok_req;
-  const int32_t* req_bt;
-  const int32_t* bt;
-  const double* inv_freq;  // [hd/2] theta^(-2j/hd)
-  uint16_t* q_out;
-  uint16_t* k_pool;
-  uint16_t* v_pool;
-};
-void launch_rope_kv(hipStream_t s, const RopeKvArgs& a);
 
 // Copy k, v [n][nkv][hd] into the pool slots of positions ctx..ctx+n-1.
 void launch_append_kv(hipStream_t s, const uint16_t* k, const uint16_t* v, int n_tokens, int ctx,

@@ -50,7 +50,9 @@ struct hb_layer {
   int gemm_ksplit = 0;  // HB_GEMM_KSPLIT at creation: force one K split (testing)
   PlanOptions plan_opt;  // HB_ATTN_SPLIT_TILE / HB_ATTN_SPLIT_ITEM at creation (tuning, testing)
   // workspace
-  uint16_t *xn = nullptr, *qkv = nullptr, *q_rot = nullptr, *attn = nullptr, *mlp = nullptr;
+  uint16_t *xn = nullptr, *q_rot = nullptr, *attn = nullptr, *mlp = nullptr;
+  float* rope_cs = nullptr;    // [max_T][hd]: per-token cos | sin (RoPE)
+  int32_t* tok_slot = nullptr; // [max_T]: pool block * 16 + slot of each new token
   float* h2 = nullptr;
   double* inv_freq = nullptr;
   float *part_o = nullptr, *part_ml = nullptr;
@@ -189,7 +191,7 @@ hb_status timed(hb_layer* L, int kernel, F&& launch) {
 void free_layer(hb_layer* L) {
   if (!L) return;
   (void)hipStreamSynchronize(L->stream);
-  for (void* p : {(void*)L->xn, (void*)L->qkv, (void*)L->q_rot, (void*)L->attn, (void*)L->mlp, (void*)L->h2,
+  for (void* p : {(void*)L->xn, (void*)L->rope_cs, (void*)L->tok_slot, (void*)L->q_rot, (void*)L->attn, (void*)L->mlp, (void*)L->h2,
                   (void*)L->inv_freq, (void*)L->part_o, (void*)L->part_ml, (void*)L->meta, (void*)L->splitk})
     if (p) (void)hipFree(p);
   for (Stage& s : L->stage) {
@@ -221,7 +223,10 @@ hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
   gq.A = L->xn; gq.lda = d.H;
   gq.B = static_cast<const uint16_t*>(L->w.w_qkv); gq.ldb = d.H;
   gq.M = T; gq.N = d.qkv_n; gq.K = d.H;
-  gq.C = L->qkv; gq.ldc = d.qkv_n; gq.epi = GEMM_STORE_BF16;
+  gq.C = L->q_rot; gq.ldc = d.nq * d.hd; gq.epi = GEMM_QKV_ROPE;
+  gq.rope_cs = L->rope_cs; gq.tok_slot = L->tok_slot;
+  gq.k_pool = static_cast<uint16_t*>(L->pool.k_pool); gq.v_pool = static_cast<uint16_t*>(L->pool.v_pool);
+  gq.nq = d.nq; gq.nkv = d.nkv; gq.hd = d.hd;
 
   go.A = L->attn; go.lda = d.nq * d.hd;
   go.B = static_cast<const uint16_t*>(L->w.w_o); go.ldb = d.nq * d.hd;
@@ -256,31 +261,27 @@ hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
   if (st != HB_OK) return st;
   const int32_t* meta = L->meta;
 
+  RopePrep rp{};
+  rp.tok_pos = meta + p.off_tok_pos; rp.tok_req = meta + p.off_tok_req;
+  rp.req_bt = meta + p.off_req_bt; rp.bt = meta + p.off_bt;
+  rp.inv_freq = L->inv_freq; rp.hd = d.hd; rp.cs = L->rope_cs; rp.slot = L->tok_slot;
   st = timed(L, HB_K_RMSNORM_ATTN, [&] {
-    launch_rmsnorm(s, x_in, false, static_cast<const uint16_t*>(L->w.g_attn), L->xn, T, d.H, d.eps);
+    launch_rmsnorm(s, x_in, false, static_cast<const uint16_t*>(L->w.g_attn), L->xn, T, d.H, d.eps, &rp);
   });
   if (st != HB_OK) return st;
+  // q, k rotated and k, v scattered into the pool by the epilogue
   st = timed(L, HB_K_GEMM_QKV, [&] { launch_gemm(s, gq, pq, L->splitk); });
-  if (st != HB_OK) return st;
-
-  RopeKvArgs r{};
-  r.qkv = L->qkv; r.T = T; r.nq = d.nq; r.nkv = d.nkv; r.hd = d.hd;
-  r.tok_pos = meta + p.off_tok_pos; r.tok_req = meta + p.off_tok_req;
-  r.req_bt = meta + p.off_req_bt; r.bt = meta + p.off_bt;
-  r.inv_freq = L->inv_freq; r.q_out = L->q_rot;
-  r.k_pool = static_cast<uint16_t*>(L->pool.k_pool); r.v_pool = static_cast<uint16_t*>(L->pool.v_pool);
-  st = timed(L, HB_K_ROPE_KV, [&] { launch_rope_kv(s, r); });
   if (st != HB_OK) return st;
 
   AttnArgs at{};
   at.q = L->q_rot; at.o = L->attn;
-  at.k_pool = r.k_pool; at.v_pool = r.v_pool;
+  at.k_pool = gq.k_pool; at.v_pool = gq.v_pool;
   at.tiles = meta + p.off_tiles;
   at.items = meta + p.off_items; at.n_items = p.n_items;
   at.units = meta + p.off_units; at.n_units = p.n_units;
   at.groups = meta + p.off_groups; at.n_groups = p.n_groups;
   at.merge_units = meta + p.off_merge; at.n_merge_units = p.n_merge_units;
-  at.req_bt = r.req_bt; at.bt = r.bt;
+  at.req_bt = rp.req_bt; at.bt = rp.bt;
   at.part_o = L->part_o; at.part_ml = L->part_ml;
   at.nq = d.nq; at.nkv = d.nkv; at.hd = d.hd;
   at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.hd));
@@ -358,7 +359,8 @@ hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w,
   if (const char* e = std::getenv("HB_ATTN_UNIT_BLOCK")) L->plan_opt.unit_block = std::atoi(e);
   const size_t T = d.max_T;
   struct Alloc { void** p; size_t bytes; } allocs[] = {
-      {(void**)&L->xn, T * d.H * 2},         {(void**)&L->qkv, T * d.qkv_n * 2},
+      {(void**)&L->xn, T * d.H * 2},         {(void**)&L->rope_cs, T * d.hd * 4},
+      {(void**)&L->tok_slot, T * 4},
       {(void**)&L->q_rot, T * d.nq * d.hd * 2}, {(void**)&L->attn, T * d.nq * d.hd * 2},
       {(void**)&L->mlp, T * d.F * 2},        {(void**)&L->h2, T * d.H * 4},
       {(void**)&L->inv_freq, (size_t)d.hd / 2 * sizeof(double)},
@@ -437,7 +439,7 @@ hb_status hb_kernel_times(hb_layer* L, double* total_ms, int64_t* launches, int3
 }
 
 const char* hb_kernel_name(int32_t k) {
-  static const char* names[HB_K_COUNT] = {"rmsnorm_attn", "gemm_qkv",  "rope_kv",        "attention", "attn_merge",
+  static const char* names[HB_K_COUNT] = {"rmsnorm_attn", "gemm_qkv",  "attention", "attn_merge",
                                           "gemm_o",       "rmsnorm_ffn", "gemm_gate_up", "gemm_down"};
   return (k >= 0 && k < HB_K_COUNT) ? names[k] : "unknown";
 }

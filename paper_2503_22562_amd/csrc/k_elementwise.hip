@@ -1,5 +1,5 @@
-// Bandwidth-bound kernels of the layer: RMSNorm, RoPE + paged KV scatter,
-// the KV append copy, and the profiling fills.
+// Bandwidth-bound kernels of the layer: RMSNorm (with the RoPE inputs of the
+// QKV epilogue), the KV append copy, and the profiling fills.
 #include "hb_device.h"
 #include "hb_kernels.h"
 
@@ -8,12 +8,30 @@ namespace hb {
 // ---------------------------------------------------------------------------
 // RMSNorm: one 256-thread workgroup per token row; each thread holds up to
 // MAXV vectors of 8 elements in registers between the reduction and the scale.
+// ROPE: the workgroup also writes the token's RoPE cos/sin row and pool slot
+// for the QKV epilogue (angles formed and reduced mod 2 pi in fp64, evaluated
+// in fp32).
 // ---------------------------------------------------------------------------
-template <bool F32IN, int MAXV>
+template <bool F32IN, int MAXV, bool ROPE>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const void* __restrict__ x, const uint16_t* __restrict__ g,
-                                                      uint16_t* __restrict__ out, int H, float eps) {
+                                                      uint16_t* __restrict__ out, int H, float eps, RopePrep rp) {
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x;
+  if (ROPE) {
+    const int p = rp.tok_pos[row];
+    const int half = rp.hd >> 1;
+    if (tid < half) {
+      const double ang = (double)p * rp.inv_freq[tid];
+      const double r = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
+      float sv, cv;
+      sincosf((float)r, &sv, &cv);
+      rp.cs[(size_t)row * rp.hd + tid] = cv;
+      rp.cs[(size_t)row * rp.hd + half + tid] = sv;
+    } else if (tid == half) {
+      const int blk = rp.bt[rp.req_bt[rp.tok_req[row]] + (p >> 4)];
+      rp.slot[row] = blk * 16 + (p & 15);
+    }
+  }
   const int nvec = H >> 3;
   float v[MAXV][8];
   float ss = 0.f;
@@ -51,83 +69,22 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const void* __restrict__ x
   }
 }
 
+template <int MAXV>
+static void launch_rmsnorm_v(hipStream_t s, const void* x, bool x_f32, const uint16_t* g, uint16_t* out, int T, int H,
+                             float eps, const RopePrep* rope) {
+  const RopePrep rp = rope ? *rope : RopePrep{};
+  if (rope) rmsnorm_kernel<false, MAXV, true><<<T, 256, 0, s>>>(x, g, out, H, eps, rp);
+  else if (x_f32) rmsnorm_kernel<true, MAXV, false><<<T, 256, 0, s>>>(x, g, out, H, eps, rp);
+  else rmsnorm_kernel<false, MAXV, false><<<T, 256, 0, s>>>(x, g, out, H, eps, rp);
+}
+
 void launch_rmsnorm(hipStream_t s, const void* x, bool x_f32, const uint16_t* g, uint16_t* out, int T, int H,
-                    float eps) {
+                    float eps, const RopePrep* rope) {
   if (T <= 0) return;
   const int nvec = H / 8;
-  if (nvec <= 256) {
-    if (x_f32) rmsnorm_kernel<true, 1><<<T, 256, 0, s>>>(x, g, out, H, eps);
-    else rmsnorm_kernel<false, 1><<<T, 256, 0, s>>>(x, g, out, H, eps);
-  } else if (nvec <= 1024) {
-    if (x_f32) rmsnorm_kernel<true, 4><<<T, 256, 0, s>>>(x, g, out, H, eps);
-    else rmsnorm_kernel<false, 4><<<T, 256, 0, s>>>(x, g, out, H, eps);
-  } else {
-    if (x_f32) rmsnorm_kernel<true, 8><<<T, 256, 0, s>>>(x, g, out, H, eps);
-    else rmsnorm_kernel<false, 8><<<T, 256, 0, s>>>(x, g, out, H, eps);
-  }
-}
-
-// ---------------------------------------------------------------------------
-// RoPE + KV scatter: one workgroup per token. Angles p * theta^(-2j/hd) are
-// formed and reduced modulo 2 pi in fp64, then evaluated in fp32. A work
-// item rotates 8 dimension pairs (j, j + hd/2) of one q or k head with 16-byte
-// loads and stores. K goes to k_pool[blk][g][slot][d], V to
-// v_pool[blk][g][slot/4][d][slot%4].
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void rope_kv_kernel(RopeKvArgs a) {
-  __shared__ float cs[64], sn[64];
-  const int t = blockIdx.x, tid = threadIdx.x;
-  const int hd = a.hd, half = hd >> 1, hv = half >> 3;
-  const int p = a.tok_pos[t];
-  if (tid < half) {
-    // angle formed and reduced to [-pi, pi] in fp64, then evaluated in fp32
-    // (the rotation itself is fp32, and its inputs and outputs bf16)
-    const double ang = (double)p * a.inv_freq[tid];
-    const double r = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
-    float sv, cv;
-    sincosf((float)r, &sv, &cv);
-    cs[tid] = cv;
-    sn[tid] = sv;
-  }
-  const int blk = a.bt[a.req_bt[a.tok_req[t]] + (p >> 4)];
-  const int slot = p & 15;
-  __syncthreads();
-  const uint16_t* row = a.qkv + (size_t)t * (a.nq + 2 * a.nkv) * hd;
-  // q heads 0..nq-1, then k heads (the row holds them contiguously)
-  for (int idx = tid; idx < (a.nq + a.nkv) * hv; idx += 256) {
-    const int h = idx / hv, j0 = 8 * (idx - h * hv);
-    const u32x4 lo = ld16(row + h * hd + j0), hi = ld16(row + h * hd + half + j0);
-    u32x4 r0, r1;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int j = j0 + 2 * e;
-      const float u0 = bf16_lo(lo[e]), u1 = bf16_hi(lo[e]), w0 = bf16_lo(hi[e]), w1 = bf16_hi(hi[e]);
-      r0[e] = pack_bf16x2(u0 * cs[j] - w0 * sn[j], u1 * cs[j + 1] - w1 * sn[j + 1]);
-      r1[e] = pack_bf16x2(w0 * cs[j] + u0 * sn[j], w1 * cs[j + 1] + u1 * sn[j + 1]);
-    }
-    uint16_t* dst = (h < a.nq) ? a.q_out + ((size_t)t * a.nq + h) * hd
-                               : a.k_pool + (((size_t)blk * a.nkv + (h - a.nq)) * 16 + slot) * hd;
-    st16(dst + j0, r0);
-    st16(dst + half + j0, r1);
-  }
-  // values -> v_pool (dim-major inside each group of four slots)
-  const uint16_t* vrow = row + (a.nq + a.nkv) * hd;
-  const int dv = hd >> 3;
-  for (int idx = tid; idx < a.nkv * dv; idx += 256) {
-    const int g = idx / dv, d0 = 8 * (idx - g * dv);
-    const u32x4 v = ld16(vrow + g * hd + d0);
-    uint16_t* dst = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * hd + ((slot >> 2) * hd + d0) * 4 + (slot & 3);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      dst[8 * e] = (uint16_t)(v[e] & 0xFFFFu);
-      dst[8 * e + 4] = (uint16_t)(v[e] >> 16);
-    }
-  }
-}
-
-void launch_rope_kv(hipStream_t s, const RopeKvArgs& a) {
-  if (a.T <= 0) return;
-  rope_kv_kernel<<<a.T, 256, 0, s>>>(a);
+  if (nvec <= 256) launch_rmsnorm_v<1>(s, x, x_f32, g, out, T, H, eps, rope);
+  else if (nvec <= 1024) launch_rmsnorm_v<4>(s, x, x_f32, g, out, T, H, eps, rope);
+  else launch_rmsnorm_v<8>(s, x, x_f32, g, out, T, H, eps, rope);
 }
 
 // ---------------------------------------------------------------------------

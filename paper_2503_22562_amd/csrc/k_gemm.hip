@@ -243,6 +243,53 @@ __device__ __forceinline__ void interleave_reads() {
   if (extra > 0) __builtin_amdgcn_sched_group_barrier(0x008, extra, 0);
 }
 
+// QKV epilogue of one accumulator row (TN fragments of 4 columns, starting at
+// a head boundary nbase): q and k heads are rotated pairwise (column j with
+// j + hd/2, PAIR = hd/32 fragments apart, both in this lane) with the row's
+// cos/sin; q is stored to C, k and v to the token's pool slot.
+template <int TN, int PAIR>
+__device__ __forceinline__ void qkv_rope_row(const GemmArgs& a, const f32x4 (&acc)[TN], int m, int nbase, int cq) {
+  constexpr int HD = 32 * PAIR, HALF = HD / 2;
+  const int qk_end = (a.nq + a.nkv) * HD;
+  const int slotm = a.tok_slot[m];
+  const int blk = slotm >> 4, slot = slotm & 15;
+  const float* csr = a.rope_cs + (size_t)m * HD;
+#pragma unroll
+  for (int ni = 0; ni < TN; ++ni) {
+    const int n = nbase + 16 * ni + cq;
+    if (n >= a.N) continue;
+    if (n < qk_end) {
+      if ((ni % (2 * PAIR)) >= PAIR) continue;  // upper half: done with its partner
+      const f32x4 lo = acc[ni], hi = acc[ni + PAIR < TN ? ni + PAIR : TN - 1];
+      const int j = n % HD;
+      const u32x4 c4 = ld16(csr + j), s4 = ld16(csr + HALF + j);
+      float rl[4], rh[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float c = __uint_as_float(c4[e]), sn = __uint_as_float(s4[e]);
+        rl[e] = lo[e] * c - hi[e] * sn;
+        rh[e] = hi[e] * c + lo[e] * sn;
+      }
+      const u32x2 wl = {pack_bf16x2(rl[0], rl[1]), pack_bf16x2(rl[2], rl[3])};
+      const u32x2 wh = {pack_bf16x2(rh[0], rh[1]), pack_bf16x2(rh[2], rh[3])};
+      uint16_t* dst;
+      if (n < a.nq * HD) {
+        dst = reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + (n - j);
+      } else {
+        const int g = (n - a.nq * HD) / HD;
+        dst = a.k_pool + (((size_t)blk * a.nkv + g) * 16 + slot) * HD;
+      }
+      st8(dst + j, wl);
+      st8(dst + HALF + j, wh);
+    } else {
+      const int g = (n - qk_end) / HD, d = n % HD;
+      uint16_t* vp = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * HD + ((slot >> 2) * HD + d) * 4 + (slot & 3);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) vp[4 * e] = (uint16_t)f32_to_bf16(acc[ni][e]);
+    }
+  }
+}
+
 template <int TM, int TN, int WR, int WC, int S, int EPI>
 __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int tiles_m, int tiles_n, int ksplit,
                                                                   int kchunk, float* __restrict__ partial) {
@@ -377,6 +424,11 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
     __builtin_amdgcn_sched_barrier(0);
     const int m = m0 + wm * WM + 16 * mi + fr;
     if (m >= M) continue;
+    if (EPI == GEMM_QKV_ROPE) {
+      if (a.hd == 128) qkv_rope_row<TN, 4>(a, acc[mi], m, nt * BN + wn * WN, cq);
+      else qkv_rope_row<TN, 2>(a, acc[mi], m, nt * BN + wn * WN, cq);
+      continue;
+    }
     if (EPI == GEMM_SWIGLU) {
 #pragma unroll
       for (int ni = 0; ni < TN / 2; ++ni) {
@@ -521,16 +573,21 @@ GemmPlan plan_gemm(const GemmArgs& a, int cu_count, int force_cfg, int force_ksp
   if (a.K % 64 != 0) return best;
   double best_cost = 1e300;
   const int ksteps = a.K / 64;
+  // the QKV epilogue needs whole heads in a wave (rotation partners in one lane)
+  auto fits = [&](const TileCfg& c) { return a.epi != GEMM_QKV_ROPE || (16 * c.tn) % a.hd == 0; };
+  if (force_cfg >= 0 && (force_cfg >= kNumTiles || !fits(kTiles[force_cfg]))) force_cfg = -1;
   for (int i = 0; i < kNumTiles; ++i) {
     if (force_cfg >= 0 && i != force_cfg) continue;
     const TileCfg& c = kTiles[i];
+    if (!fits(c)) continue;
     const int bm = 16 * c.tm * c.wr, bn = 16 * c.tn * c.wc;
     const int ncols = (a.epi == GEMM_SWIGLU) ? bn / 2 : bn;
     const int tm = (a.M + bm - 1) / bm, tn = (a.N + ncols - 1) / ncols;
     const int slots = std::max(1, cu_count) * tiles_per_cu(c);
     for (int ks = 1; ks <= 8; ++ks) {
-      if (ks > 1 && (a.epi == GEMM_SWIGLU || ksteps < 4 * ks)) break;
-      if (force_ksplit > 0 && ks != force_ksplit && !(a.epi == GEMM_SWIGLU && ks == 1)) continue;
+      const bool no_split = a.epi == GEMM_SWIGLU || a.epi == GEMM_QKV_ROPE;
+      if (ks > 1 && (no_split || ksteps < 4 * ks)) break;
+      if (force_ksplit > 0 && ks != force_ksplit && !(no_split && ks == 1)) continue;
       const int kst = (ksteps + ks - 1) / ks;
       if ((ks - 1) * kst >= ksteps) continue;  // every split gets at least one stage
       const int nwg = tm * tn * ks;
@@ -554,6 +611,7 @@ void launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& p, float* par
   }
   switch (a.epi) {
     case GEMM_STORE_BF16: launch_cfg<GEMM_STORE_BF16>(p.cfg, s, a, p.tiles_m, p.tiles_n, p.ksplit, p.kchunk, partial); break;
+    case GEMM_QKV_ROPE: launch_cfg<GEMM_QKV_ROPE>(p.cfg, s, a, p.tiles_m, p.tiles_n, p.ksplit, p.kchunk, partial); break;
     case GEMM_RESIDUAL: launch_cfg<GEMM_RESIDUAL>(p.cfg, s, a, p.tiles_m, p.tiles_n, p.ksplit, p.kchunk, partial); break;
     default: launch_cfg<GEMM_SWIGLU>(p.cfg, s, a, p.tiles_m, p.tiles_n, p.ksplit, p.kchunk, partial); break;
   }

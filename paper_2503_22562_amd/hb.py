@@ -15,8 +15,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhb.so")
 
 HB_OK, HB_ERR_INVALID, HB_ERR_RANGE, HB_ERR_OOM, HB_ERR_HIP, HB_ERR_UNSUPPORTED = range(6)
 HB_OUT_F32, HB_OUT_BF16 = 0, 1
-(HB_K_RMSNORM_ATTN, HB_K_GEMM_QKV, HB_K_ROPE_KV, HB_K_ATTENTION, HB_K_ATTN_MERGE, HB_K_GEMM_O,
- HB_K_RMSNORM_FFN, HB_K_GEMM_GATE_UP, HB_K_GEMM_DOWN, HB_K_COUNT) = range(10)
+(HB_K_RMSNORM_ATTN, HB_K_GEMM_QKV, HB_K_ATTENTION, HB_K_ATTN_MERGE, HB_K_GEMM_O,
+ HB_K_RMSNORM_FFN, HB_K_GEMM_GATE_UP, HB_K_GEMM_DOWN, HB_K_COUNT) = range(9)
 HB_STAGE_Q, HB_STAGE_ATTN, HB_STAGE_H2, HB_STAGE_MLP = range(4)
 
 EXPORTED = ("hb_create_layer", "hb_destroy_layer", "hb_append_kv", "hb_run_iteration", "hb_validate_batch",
