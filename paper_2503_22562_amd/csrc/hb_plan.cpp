@@ -167,12 +167,16 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p,
   // split lengths (multiples of 64 keys): about one round of tile workgroups
   // (each split also writes kTileCols columns of fp32 partials) and about four
   // items per wave slot (8 per compute unit), so long decodes do not set the
-  // finishing time
+  // finishing time. When both kinds are present, tiles run beside the
+  // bandwidth-bound items for the whole launch, so they are split less
+  // (4096 keys), and items are at least 512 keys: both halve the partial
+  // results the merge must read (measured on MI355X over chunk/decode mixes).
   const int cus = std::max(1, cu_count);
+  const bool mixed = tile_keys > 0 && item_keys > 0;
   const int S_t = opt.split_tile > 0 ? round_up(opt.split_tile, 64)
-                                     : std::max(1024, round_up((int64_t)(tile_keys / (1.0 * cus)) + 1, 64));
+                                     : std::max(mixed ? 4096 : 1024, round_up((int64_t)(tile_keys / (1.0 * cus)) + 1, 64));
   const int S_i = opt.split_item > 0 ? round_up(opt.split_item, 64)
-                                     : std::max(256, round_up((int64_t)(item_keys / (32.0 * cus)) + 1, 64));
+                                     : std::max(512, round_up((int64_t)(item_keys / (32.0 * cus)) + 1, 64));
   p->split_tile = S_t;
   p->split_item = S_i;
 
