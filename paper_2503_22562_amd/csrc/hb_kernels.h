@@ -58,7 +58,9 @@ struct GemmPlan {
 GemmPlan plan_gemm(const GemmArgs& a, int cu_count, int force_cfg = -1, int force_ksplit = 0);
 // Number of LDS-pipelined tile shapes (valid force_cfg values are 0..count-1).
 int gemm_tile_count();
-// `partial` holds ksplit * M * N fp32 when plan.ksplit > 1.
+// Columns of one row of split-K partial sums (gate/up: 2 N, gate then up).
+int partial_width(const GemmArgs& a);
+// `partial` holds ksplit * M * partial_width(a) fp32 when plan.ksplit > 1.
 void launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& plan, float* partial);
 
 // Copy k, v [n][nkv][hd] into the pool slots of positions ctx..ctx+n-1.

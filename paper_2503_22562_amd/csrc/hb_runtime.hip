@@ -250,8 +250,9 @@ hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
   const GemmPlan pu = plan_gemm(gu, L->cu_count, L->gemm_tile, L->gemm_ksplit),
                  pd = plan_gemm(gd, L->cu_count, L->gemm_tile, L->gemm_ksplit);
   size_t sk = 0;
-  for (const auto& [pl, ga] : {std::make_pair(pq, gq), std::make_pair(po, go), std::make_pair(pd, gd)})
-    if (pl.ksplit > 1) sk = std::max(sk, (size_t)pl.ksplit * ga.M * ga.N);
+  for (const auto& [pl, ga] : {std::make_pair(pq, gq), std::make_pair(po, go), std::make_pair(pu, gu),
+                                std::make_pair(pd, gd)})
+    if (pl.ksplit > 1) sk = std::max(sk, (size_t)pl.ksplit * ga.M * partial_width(ga));
 
   hb_status st = ensure_meta(L, p.meta.size());
   if (st == HB_OK) st = ensure_parts(L, p.n_slots);

@@ -424,6 +424,27 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
     __builtin_amdgcn_sched_barrier(0);
     const int m = m0 + wm * WM + 16 * mi + fr;
     if (m >= M) continue;
+    if (ksplit > 1) {
+      // fp32 partial sums, rows of partial_width(N) columns: the reduce
+      // kernel applies the epilogue (SwiGLU: gate at n, up at N + n)
+      const int W = (EPI == GEMM_SWIGLU) ? 2 * N : N;
+      float* prow = partial + ((size_t)ks * M + m) * W;
+#pragma unroll
+      for (int ni = 0; ni < TN; ++ni) {
+        int n, col;
+        if (EPI == GEMM_SWIGLU) {
+          n = nt * (BN / 2) + wn * (WN / 2) + 16 * (ni % (TN / 2)) + cq;
+          col = ni < TN / 2 ? n : N + n;
+        } else {
+          n = nt * BN + wn * WN + 16 * ni + cq;
+          col = n;
+        }
+        if (n >= N) continue;
+        const f32x4 c = acc[mi][ni];
+        st16(prow + col, u32x4{__float_as_uint(c[0]), __float_as_uint(c[1]), __float_as_uint(c[2]), __float_as_uint(c[3])});
+      }
+      continue;
+    }
     if (EPI == GEMM_QKV_ROPE) {
       if (a.hd == 128) qkv_rope_row<TN, 4>(a, acc[mi], m, nt * BN + wn * WN, cq);
       else qkv_rope_row<TN, 2>(a, acc[mi], m, nt * BN + wn * WN, cq);
@@ -446,11 +467,6 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
         const int n = nt * BN + wn * WN + 16 * ni + cq;
         if (n >= N) continue;
         f32x4 c = acc[mi][ni];
-        if (ksplit > 1) {
-          u32x4 o = {__float_as_uint(c[0]), __float_as_uint(c[1]), __float_as_uint(c[2]), __float_as_uint(c[3])};
-          st16(partial + ((size_t)ks * M + m) * N + n, o);
-          continue;
-        }
         if (EPI == GEMM_RESIDUAL) {
           if (a.r_f32) {
             const u32x4 rr = ld16(reinterpret_cast<const float*>(a.R) + (size_t)m * a.ldr + n);
@@ -473,18 +489,71 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
   }
 }
 
-// Sum of the split-K partials in split order, then the epilogue.
+// Sum of the split-K partials in split order, then the GEMM's epilogue: for
+// the QKV GEMM the RoPE rotation of q and k and the pool scatter of k and v
+// (one work item = 4 columns of a row, with their rotation partners), for
+// gate/up the SwiGLU product, else the residual add and the store.
+template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int ksplit, const float* __restrict__ partial) {
+  const int W = (EPI == GEMM_SWIGLU) ? 2 * a.N : a.N;
+  const size_t split_stride = (size_t)a.M * W;
+  auto sum4 = [&](int m, int n) {
+    f32x4 c = {0.f, 0.f, 0.f, 0.f};
+    const float* p = partial + (size_t)m * W + n;
+    for (int s = 0; s < ksplit; ++s) {
+      const u32x4 v = ld16(p + s * split_stride);
+      for (int j = 0; j < 4; ++j) c[j] += __uint_as_float(v[j]);
+    }
+    return c;
+  };
+  const int64_t step = (int64_t)gridDim.x * 256;
+  if (EPI == GEMM_QKV_ROPE) {
+    const int hd = a.hd, half = hd / 2, qk_heads = a.nq + a.nkv;
+    const int qk_units = qk_heads * (half / 4), per_row = qk_units + a.nkv * (hd / 4);
+    const int64_t total = (int64_t)a.M * per_row;
+    for (int64_t v = blockIdx.x * 256ll + threadIdx.x; v < total; v += step) {
+      const int m = (int)(v / per_row);
+      int r = (int)(v - (int64_t)m * per_row);
+      const int slotm = a.tok_slot[m];
+      const int blk = slotm >> 4, slot = slotm & 15;
+      if (r < qk_units) {
+        const int h = r / (half / 4), j = (r - h * (half / 4)) * 4;
+        const f32x4 lo = sum4(m, h * hd + j), hi = sum4(m, h * hd + half + j);
+        const float* csr = a.rope_cs + (size_t)m * hd;
+        const u32x4 c4 = ld16(csr + j), s4 = ld16(csr + half + j);
+        float rl[4], rh[4];
+        for (int e = 0; e < 4; ++e) {
+          const float c = __uint_as_float(c4[e]), sn = __uint_as_float(s4[e]);
+          rl[e] = lo[e] * c - hi[e] * sn;
+          rh[e] = hi[e] * c + lo[e] * sn;
+        }
+        uint16_t* dst = h < a.nq ? reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + h * hd
+                                 : a.k_pool + (((size_t)blk * a.nkv + (h - a.nq)) * 16 + slot) * hd;
+        st8(dst + j, u32x2{pack_bf16x2(rl[0], rl[1]), pack_bf16x2(rl[2], rl[3])});
+        st8(dst + half + j, u32x2{pack_bf16x2(rh[0], rh[1]), pack_bf16x2(rh[2], rh[3])});
+      } else {
+        r -= qk_units;
+        const int g = r / (hd / 4), d = (r - g * (hd / 4)) * 4;
+        const f32x4 c = sum4(m, (qk_heads + g) * hd + d);
+        uint16_t* vp = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * hd + ((slot >> 2) * hd + d) * 4 + (slot & 3);
+        for (int e = 0; e < 4; ++e) vp[4 * e] = (uint16_t)f32_to_bf16(c[e]);
+      }
+    }
+    return;
+  }
   const int64_t nvec = (int64_t)a.M * a.N / 4;
-  for (int64_t v = blockIdx.x * 256ll + threadIdx.x; v < nvec; v += (int64_t)gridDim.x * 256) {
+  for (int64_t v = blockIdx.x * 256ll + threadIdx.x; v < nvec; v += step) {
     const int64_t e = v * 4;
     const int m = (int)(e / a.N), n = (int)(e - (int64_t)m * a.N);
-    f32x4 c = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < ksplit; ++s) {
-      const u32x4 p = ld16(partial + ((size_t)s * a.M + m) * a.N + n);
-      for (int j = 0; j < 4; ++j) c[j] += __uint_as_float(p[j]);
+    f32x4 c = sum4(m, n);
+    if (EPI == GEMM_SWIGLU) {
+      const f32x4 up = sum4(m, a.N + n);
+      const u32x2 o = {pack_bf16x2(silu_f(c[0]) * up[0], silu_f(c[1]) * up[1]),
+                       pack_bf16x2(silu_f(c[2]) * up[2], silu_f(c[3]) * up[3])};
+      st8(reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + n, o);
+      continue;
     }
-    if (a.epi == GEMM_RESIDUAL) {
+    if (EPI == GEMM_RESIDUAL) {
       if (a.r_f32) {
         const u32x4 rr = ld16(reinterpret_cast<const float*>(a.R) + (size_t)m * a.ldr + n);
         for (int j = 0; j < 4; ++j) c[j] += __uint_as_float(rr[j]);
@@ -494,7 +563,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int kspl
         c[2] += bf16_lo(rr[1]); c[3] += bf16_hi(rr[1]);
       }
     }
-    if (a.epi == GEMM_RESIDUAL && a.c_f32) {
+    if (EPI == GEMM_RESIDUAL && a.c_f32) {
       u32x4 o = {__float_as_uint(c[0]), __float_as_uint(c[1]), __float_as_uint(c[2]), __float_as_uint(c[3])};
       st16(reinterpret_cast<float*>(a.C) + (size_t)m * a.ldc + n, o);
     } else {
@@ -503,7 +572,6 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int kspl
     }
   }
 }
-
 
 }  // namespace gemm_detail
 
@@ -517,12 +585,13 @@ struct TileCfg {
 // Accumulators and both fragment sets stay within the 256 VGPRs of a wave.
 // 8-wave workgroups put two waves on each SIMD; 4-wave ones with LDS rings
 // of at most 80 KB run two workgroups per CU. The costs were fitted to
-// MI355X timings of the layer's four GEMMs over M = 384..2304.
+// MI355X timings of the layer's four GEMMs over M = 384..2374.
 constexpr TileCfg kTiles[] = {
-    {8, 4, 2, 2, 3, 0.969f, 2.6f},  {4, 8, 2, 2, 3, 0.999f, 1.0f}, {4, 4, 2, 2, 2, 0.892f, 6.9f},
-    {6, 4, 2, 2, 2, 1.019f, 17.9f}, {3, 8, 2, 2, 3, 0.842f, 2.1f}, {9, 4, 2, 2, 3, 1.095f, 1.8f},
-    {2, 8, 2, 2, 3, 0.744f, 0.0f},  {8, 4, 2, 4, 2, 1.295f, 15.8f}, {6, 4, 2, 4, 2, 1.323f, 0.2f},
-    {4, 4, 2, 4, 3, 0.864f, 7.3f},
+    {8, 4, 2, 2, 3, 0.983f, 3.8f},  {4, 8, 2, 2, 3, 0.990f, 1.9f},  {4, 4, 2, 2, 2, 0.902f, 4.7f},
+    {6, 4, 2, 2, 2, 1.018f, 15.3f}, {3, 8, 2, 2, 3, 0.833f, 1.8f},  {9, 4, 2, 2, 3, 1.087f, 1.3f},
+    {2, 8, 2, 2, 3, 0.736f, 0.0f},  {8, 4, 2, 4, 2, 1.287f, 13.1f}, {6, 4, 2, 4, 2, 1.289f, 0.0f},
+    {4, 4, 2, 4, 3, 0.855f, 5.2f},  {4, 8, 4, 2, 2, 1.282f, 13.5f}, {3, 8, 4, 2, 2, 1.274f, 1.6f},
+    {2, 8, 4, 2, 3, 0.853f, 6.4f},
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 
@@ -552,12 +621,17 @@ void launch_cfg(int idx, hipStream_t s, const GemmArgs& a, int tm, int tn, int k
     case 6: launch_tile<2, 8, 2, 2, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
     case 7: launch_tile<8, 4, 2, 4, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
     case 8: launch_tile<6, 4, 2, 4, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
-    default: launch_tile<4, 4, 2, 4, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 9: launch_tile<4, 4, 2, 4, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 10: launch_tile<4, 8, 4, 2, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 11: launch_tile<3, 8, 4, 2, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    default: launch_tile<2, 8, 4, 2, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
   }
 }
 }  // namespace
 
 int gemm_tile_count() { return kNumTiles; }
+
+int partial_width(const GemmArgs& a) { return a.epi == GEMM_SWIGLU ? 2 * a.N : a.N; }
 
 // Cost model (microseconds): workgroups run in rounds of one (two, for small
 // LDS rings) per CU, each round costing its K stages at the tile's measured
@@ -568,32 +642,31 @@ static int tiles_per_cu(const TileCfg& c) {
   return (c.wr * c.wc == 4 && 2 * lds <= 160 * 1024) ? 2 : 1;
 }
 
-GemmPlan plan_gemm(const GemmArgs& a, int cu_count, int force_cfg, int force_ksplit) {
+static GemmPlan search_plan(const GemmArgs& a, int cu_count, int force_cfg, int force_ksplit) {
   GemmPlan best{-1, 0, 0, 1, 0};
-  if (a.K % 64 != 0) return best;
   double best_cost = 1e300;
   const int ksteps = a.K / 64;
-  // the QKV epilogue needs whole heads in a wave (rotation partners in one lane)
-  auto fits = [&](const TileCfg& c) { return a.epi != GEMM_QKV_ROPE || (16 * c.tn) % a.hd == 0; };
-  if (force_cfg >= 0 && (force_cfg >= kNumTiles || !fits(kTiles[force_cfg]))) force_cfg = -1;
+  // the in-tile QKV epilogue needs whole heads in a wave (rotation partners in
+  // one lane); with a K split the reduce kernel rotates, and any tile fits
+  auto fits = [&](const TileCfg& c, int ks) { return a.epi != GEMM_QKV_ROPE || ks > 1 || (16 * c.tn) % a.hd == 0; };
+  const int W = partial_width(a);
   for (int i = 0; i < kNumTiles; ++i) {
     if (force_cfg >= 0 && i != force_cfg) continue;
     const TileCfg& c = kTiles[i];
-    if (!fits(c)) continue;
     const int bm = 16 * c.tm * c.wr, bn = 16 * c.tn * c.wc;
     const int ncols = (a.epi == GEMM_SWIGLU) ? bn / 2 : bn;
     const int tm = (a.M + bm - 1) / bm, tn = (a.N + ncols - 1) / ncols;
     const int slots = std::max(1, cu_count) * tiles_per_cu(c);
     for (int ks = 1; ks <= 8; ++ks) {
-      const bool no_split = a.epi == GEMM_SWIGLU || a.epi == GEMM_QKV_ROPE;
-      if (ks > 1 && (no_split || ksteps < 4 * ks)) break;
-      if (force_ksplit > 0 && ks != force_ksplit && !(no_split && ks == 1)) continue;
+      if (ks > 1 && ksteps < 4 * ks) break;
+      if (force_ksplit > 0 && ks != force_ksplit) continue;
+      if (!fits(c, ks)) continue;
       const int kst = (ksteps + ks - 1) / ks;
       if ((ks - 1) * kst >= ksteps) continue;  // every split gets at least one stage
       const int nwg = tm * tn * ks;
       const int rounds = (nwg + slots - 1) / slots;
       double cost = rounds * (kst * c.stage_us + c.fixed_us);
-      if (ks > 1) cost += (double)a.M * a.N * 4.0 * (2 * ks + 1) / 5e6 + 3.0;
+      if (ks > 1) cost += (double)a.M * W * 4.0 * (2 * ks + 1) / 6e6 + 0.7;
       if (cost < best_cost * 0.999) {
         best_cost = cost;
         best = GemmPlan{i, tm, tn, ks, kst * 64};
@@ -601,6 +674,17 @@ GemmPlan plan_gemm(const GemmArgs& a, int cu_count, int force_cfg, int force_ksp
     }
   }
   return best;
+}
+
+GemmPlan plan_gemm(const GemmArgs& a, int cu_count, int force_cfg, int force_ksplit) {
+  if (a.K % 64 != 0) return GemmPlan{-1, 0, 0, 1, 0};
+  if (force_cfg >= kNumTiles) force_cfg = -1;
+  // a forced shape or split that cannot run this GEMM is relaxed: first the
+  // split, then the shape
+  GemmPlan p = search_plan(a, cu_count, force_cfg, force_ksplit);
+  if (p.cfg < 0) p = search_plan(a, cu_count, force_cfg, 0);
+  if (p.cfg < 0) p = search_plan(a, cu_count, -1, 0);
+  return p;
 }
 
 void launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& p, float* partial) {
@@ -616,9 +700,16 @@ void launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& p, float* par
     default: launch_cfg<GEMM_SWIGLU>(p.cfg, s, a, p.tiles_m, p.tiles_n, p.ksplit, p.kchunk, partial); break;
   }
   if (p.ksplit > 1) {
-    const int64_t nvec = (int64_t)a.M * a.N / 4;
-    const int grid = (int)std::min<int64_t>((nvec + 255) / 256, 8192);
-    splitk_reduce_kernel<<<grid, 256, 0, s>>>(a, p.ksplit, partial);
+    const int64_t items = a.epi == GEMM_QKV_ROPE
+                              ? (int64_t)a.M * ((a.nq + a.nkv) * (a.hd / 8) + a.nkv * (a.hd / 4))
+                              : (int64_t)a.M * a.N / 4;
+    const int grid = (int)std::min<int64_t>((items + 255) / 256, 8192);
+    switch (a.epi) {
+      case GEMM_QKV_ROPE: splitk_reduce_kernel<GEMM_QKV_ROPE><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
+      case GEMM_SWIGLU: splitk_reduce_kernel<GEMM_SWIGLU><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
+      case GEMM_RESIDUAL: splitk_reduce_kernel<GEMM_RESIDUAL><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
+      default: splitk_reduce_kernel<GEMM_STORE_BF16><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
+    }
   }
 }
 

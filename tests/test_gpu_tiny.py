@@ -244,11 +244,15 @@ def test_bf16_output_matches_fp32_output(hb):
     assert torch.equal(y16, ref)
 
 
-@pytest.mark.parametrize("tile", list(range(10)))
-@pytest.mark.parametrize("ksplit", [1, 2])
+@pytest.mark.parametrize("tile", list(range(13)))
+@pytest.mark.parametrize("ksplit", [1, 2, 3])
 def test_every_gemm_tile_shape(hb, monkeypatch, tile, ksplit):
-    """Each LDS-pipelined GEMM tile shape (and a split K) through whole-layer
-    parity; all four GEMMs here have K % 64 == 0 and ragged M and N tails."""
+    """Each LDS-pipelined GEMM tile shape, whole K or split (the split-K
+    reduce then applies RoPE + pool scatter, SwiGLU or the residual add),
+    through whole-layer parity and the q / SwiGLU stages; all four GEMMs here
+    have K % 64 == 0 and ragged M and N tails."""
+    from paper_2503_22562_amd import hb as H
+    from paper_2503_22562_amd.harness import bf16_bits
     monkeypatch.setenv("HB_GEMM_TILE", str(tile))
     monkeypatch.setenv("HB_GEMM_KSPLIT", str(ksplit))
     shape = LayerShape("gemm-tiles", 1024, 8, 2, 128, 1472, weight_seed=21)
@@ -256,6 +260,11 @@ def test_every_gemm_tile_shape(hb, monkeypatch, tile, ksplit):
     b = make_batch(shape, lens, seed=31, num_blocks=64)
     dl, w = _setup(hb, b)
     y = _run(dl, b)
-    ref = oracle_for_batch(b, oracle.weights_to_f64(w))
+    ref, st = oracle_for_batch(b, oracle.weights_to_f64(w), stages=True)
     print(f"tile {tile} ksplit {ksplit}", errors(y, ref))
     assert_parity(y, ref)
+    T = b.n_tokens
+    q = oracle.bf16_bits_to_f64(bf16_bits(dl.stage(H.HB_STAGE_Q, T)))
+    assert_stage(q, st["q"].reshape(T, -1), "q after RoPE")
+    m = oracle.bf16_bits_to_f64(bf16_bits(dl.stage(H.HB_STAGE_MLP, T)))
+    assert_stage(m, st["m"], "silu(gate)*up")
