@@ -35,7 +35,12 @@ enum GemmEpilogue { GEMM_STORE_BF16 = 0, GEMM_RESIDUAL = 1, GEMM_SWIGLU = 2, GEM
 //   GEMM_QKV_ROPE:   the columns are [q heads | k heads | v heads] of head_dim
 //                    each; q and k are rotated (rotate-half RoPE with the
 //                    per-row cos/sin of rope_cs), q goes to C [M][nq*hd], k
-//                    and v to the paged pool slot tok_slot[m] (no K split)
+//                    and v to the paged pool slot tok_slot[m]
+// With a K split, the reduce kernel applies the epilogue. GEMM_RESIDUAL with
+// fp32 C and norm_out set: the reduce also writes the RMSNorm of each C row
+// (gain norm_g, epsilon norm_eps) to norm_out bf16 [M][N], one workgroup per
+// row (launch_gemm then returns true; without a split it returns false and
+// the caller normalises).
 struct GemmArgs {
   const uint16_t* A; int lda;
   const uint16_t* B; int ldb;
@@ -47,6 +52,8 @@ struct GemmArgs {
   const float* rope_cs; const int32_t* tok_slot;
   uint16_t* k_pool; uint16_t* v_pool;
   int nq, nkv, hd;
+  // GEMM_RESIDUAL with a K split only: fused RMSNorm of the output rows
+  const uint16_t* norm_g; uint16_t* norm_out; float norm_eps;
 };
 // Tile shape, grid and K split chosen for one GEMM (cfg < 0: the
 // register-staged kernel, used when K is not a multiple of 64).
@@ -61,7 +68,8 @@ int gemm_tile_count();
 // Columns of one row of split-K partial sums (gate/up: 2 N, gate then up).
 int partial_width(const GemmArgs& a);
 // `partial` holds ksplit * M * partial_width(a) fp32 when plan.ksplit > 1.
-void launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& plan, float* partial);
+// Returns true when the RMSNorm of the output rows was fused (see GemmArgs).
+bool launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& plan, float* partial);
 
 // Copy k, v [n][nkv][hd] into the pool slots of positions ctx..ctx+n-1.
 void launch_append_kv(hipStream_t s, const uint16_t* k, const uint16_t* v, int n_tokens, int ctx,

@@ -233,6 +233,8 @@ hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
   go.M = T; go.N = d.H; go.K = d.nq * d.hd;
   go.C = L->h2; go.ldc = d.H; go.c_f32 = 1;
   go.R = x_in; go.ldr = d.H; go.r_f32 = 0; go.epi = GEMM_RESIDUAL;
+  // with a K split, the reduce also applies the pre-FFN RMSNorm
+  go.norm_g = static_cast<const uint16_t*>(L->w.g_ffn); go.norm_out = L->xn; go.norm_eps = d.eps;
 
   gu.A = L->xn; gu.lda = d.H;
   gu.B = static_cast<const uint16_t*>(L->w.w_gate_up); gu.ldb = d.H;
@@ -292,12 +294,15 @@ hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
     st = timed(L, HB_K_ATTN_MERGE, [&] { launch_attn_merge(s, at); });
     if (st != HB_OK) return st;
   }
-  st = timed(L, HB_K_GEMM_O, [&] { launch_gemm(s, go, po, L->splitk); });
+  bool ffn_norm_done = false;
+  st = timed(L, HB_K_GEMM_O, [&] { ffn_norm_done = launch_gemm(s, go, po, L->splitk); });
   if (st != HB_OK) return st;
-  st = timed(L, HB_K_RMSNORM_FFN, [&] {
-    launch_rmsnorm(s, L->h2, true, static_cast<const uint16_t*>(L->w.g_ffn), L->xn, T, d.H, d.eps);
-  });
-  if (st != HB_OK) return st;
+  if (!ffn_norm_done) {
+    st = timed(L, HB_K_RMSNORM_FFN, [&] {
+      launch_rmsnorm(s, L->h2, true, static_cast<const uint16_t*>(L->w.g_ffn), L->xn, T, d.H, d.eps);
+    });
+    if (st != HB_OK) return st;
+  }
   st = timed(L, HB_K_GEMM_GATE_UP, [&] { launch_gemm(s, gu, pu, L->splitk); });
   if (st != HB_OK) return st;
   st = timed(L, HB_K_GEMM_DOWN, [&] { launch_gemm(s, gd, pd, L->splitk); });

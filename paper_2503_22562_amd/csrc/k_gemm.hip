@@ -243,6 +243,33 @@ __device__ __forceinline__ void interleave_reads() {
   if (extra > 0) __builtin_amdgcn_sched_group_barrier(0x008, extra, 0);
 }
 
+// Scheduling directive for the second K half: after the barrier, NLOAD
+// global-to-LDS loads (the stage S ahead) and NREAD LDS reads (the next
+// stage's first half) each follow an MFMA of this half, loads first, so the
+// MFMA pipe keeps running while they issue.
+template <int NLOAD, int NREAD, int NMFMA>
+__device__ __forceinline__ void interleave_loads_reads() {
+  constexpr int ops = NLOAD + NREAD;
+  constexpr int per_op = (ops + NMFMA - 1) / NMFMA;  // ops after each MFMA
+  constexpr int slots = (ops + per_op - 1) / per_op;
+  int loads = NLOAD, reads = NREAD;
+#pragma unroll
+  for (int i = 0; i < slots; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+#pragma unroll
+    for (int j = 0; j < per_op; ++j) {
+      if (loads > 0) {
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        --loads;
+      } else if (reads > 0) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        --reads;
+      }
+    }
+  }
+  if (NMFMA > slots) __builtin_amdgcn_sched_group_barrier(0x008, NMFMA > slots ? NMFMA - slots : 1, 0);
+}
+
 // QKV epilogue of one accumulator row (TN fragments of 4 columns, starting at
 // a head boundary nbase): q and k heads are rotated pairwise (column j with
 // j + hd/2, PAIR = hd/32 fragments apart, both in this lane) with the row's
@@ -381,6 +408,7 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
 
   // (the last stage is peeled so that every loop body is one straight block
   // in which reads and MFMAs can be interleaved)
+  const int pend = min(S, nk) - 2;
   for (int kt = 0; kt < nk - 1; ++kt) {
     const int buf = kt % S;
     const uint8_t* st = smem + buf * STAGE_BYTES;
@@ -392,19 +420,22 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
     // this buffer is fully read (second-half fragments are in registers);
     // the next stage must be complete, the later ones may stay in flight
     wait_lgkm0();
-    const int pend = min(nk - kt - 2, S - 2);
-    if (S >= 4 && pend >= 2) wait_vmcnt<(S >= 4 ? 2 * LOADS : 0)>();
+    // the prologue issued min(S, nk) stages and every iteration one more
+    // (past the end: the last stage again, into a buffer no later stage
+    // reads), so min(S, nk) - 2 stages may stay in flight
+    if (pend >= S - 2) wait_vmcnt<(S - 2) * LOADS>();
+    else if (S >= 4 && pend >= 2) wait_vmcnt<(S >= 4 ? 2 * LOADS : 0)>();
     else if (S >= 3 && pend >= 1) wait_vmcnt<(S >= 3 ? LOADS : 0)>();
     else wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
-    if (kt + S < nk)
-      issue_stage<NW, LA, LB>(smem + buf * STAGE_BYTES, A_BYTES, Abase, Bbase, aoff, boff, wave, (kt + S) * 64);
-    __builtin_amdgcn_sched_barrier(0);
-    // second K half: read the next stage's first half under the MFMAs
+    // second K half: refill this buffer with the stage S ahead and read the
+    // next stage's first half, both under this half's MFMAs
+    issue_stage<NW, LA, LB>(smem + buf * STAGE_BYTES, A_BYTES, Abase, Bbase, aoff, boff, wave,
+                            min(kt + S, nk - 1) * 64);
     const uint8_t* nx = smem + ((kt + 1) % S) * STAGE_BYTES;
     read_frags<TM, TN>(fa0, fb0, nx + a_lane, nx + b_lane, broff);
     mfma_block<TM, TN>(acc, fa1, fb1);
-    interleave_reads<TM + TN, TM * TN>();
+    interleave_loads_reads<NA + NB, TM + TN, TM * TN>();
     __builtin_amdgcn_sched_barrier(0);
   }
   if (nk > 0) {
@@ -415,6 +446,8 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
     __builtin_amdgcn_sched_barrier(0);
     mfma_block<TM, TN>(acc, fa1, fb1);
   }
+  // the loads issued past the end land in LDS before the workgroup ends
+  wait_vmcnt<0>();
 
   // epilogue: acc[mi][ni][i] = C[m][n + i]
   const int cq = fg << 2;
@@ -573,6 +606,64 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int kspl
   }
 }
 
+// Split-K reduce of the fp32 residual GEMM fused with the RMSNorm that
+// follows it: one workgroup per row sums the partials in split order, adds the
+// residual, stores the row (fp32) and normalises it into norm_out (bf16), with
+// the same element-to-thread mapping and reduction order as the RMSNorm kernel.
+template <int MAXV>
+__global__ __launch_bounds__(256) void splitk_reduce_rmsnorm_kernel(GemmArgs a, int ksplit,
+                                                                    const float* __restrict__ partial) {
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x, N = a.N;
+  const int nvec = N >> 3;
+  const size_t split_stride = (size_t)a.M * N;
+  float v[MAXV][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int vi = tid + 256 * i;
+    if (vi < nvec) {
+      const float* p = partial + (size_t)row * N + 8 * vi;
+      float c[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < ksplit; ++s) {
+        const u32x4 x0 = ld16(p + s * split_stride), x1 = ld16(p + s * split_stride + 4);
+        for (int j = 0; j < 4; ++j) { c[j] += __uint_as_float(x0[j]); c[4 + j] += __uint_as_float(x1[j]); }
+      }
+      if (a.r_f32) {
+        const float* rr = reinterpret_cast<const float*>(a.R) + (size_t)row * a.ldr + 8 * vi;
+        const u32x4 r0 = ld16(rr), r1 = ld16(rr + 4);
+        for (int j = 0; j < 4; ++j) { c[j] += __uint_as_float(r0[j]); c[4 + j] += __uint_as_float(r1[j]); }
+      } else {
+        const u32x4 rr = ld16(reinterpret_cast<const uint16_t*>(a.R) + (size_t)row * a.ldr + 8 * vi);
+        for (int j = 0; j < 4; ++j) { c[2 * j] += bf16_lo(rr[j]); c[2 * j + 1] += bf16_hi(rr[j]); }
+      }
+      float* cr = reinterpret_cast<float*>(a.C) + (size_t)row * a.ldc + 8 * vi;
+      st16(cr, u32x4{__float_as_uint(c[0]), __float_as_uint(c[1]), __float_as_uint(c[2]), __float_as_uint(c[3])});
+      st16(cr + 4, u32x4{__float_as_uint(c[4]), __float_as_uint(c[5]), __float_as_uint(c[6]), __float_as_uint(c[7])});
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        v[i][j] = c[j];
+        ss += c[j] * c[j];
+      }
+    }
+  }
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float r = 1.0f / sqrtf(tot / (float)N + a.norm_eps);
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int vi = tid + 256 * i;
+    if (vi < nvec) {
+      u32x4 gw = ld16(a.norm_g + 8 * vi), o;
+      for (int j = 0; j < 4; ++j)
+        o[j] = pack_bf16x2(v[i][2 * j] * r * bf16_lo(gw[j]), v[i][2 * j + 1] * r * bf16_hi(gw[j]));
+      st16(a.norm_out + (size_t)row * N + 8 * vi, o);
+    }
+  }
+}
+
 }  // namespace gemm_detail
 
 namespace {
@@ -687,17 +778,25 @@ GemmPlan plan_gemm(const GemmArgs& a, int cu_count, int force_cfg, int force_ksp
   return p;
 }
 
-void launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& p, float* partial) {
-  if (a.M <= 0 || a.N <= 0) return;
+bool launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& p, float* partial) {
+  if (a.M <= 0 || a.N <= 0) return false;
   if (p.cfg < 0) {
     launch_gemm_regstaged(s, a);
-    return;
+    return false;
   }
   switch (a.epi) {
     case GEMM_STORE_BF16: launch_cfg<GEMM_STORE_BF16>(p.cfg, s, a, p.tiles_m, p.tiles_n, p.ksplit, p.kchunk, partial); break;
     case GEMM_QKV_ROPE: launch_cfg<GEMM_QKV_ROPE>(p.cfg, s, a, p.tiles_m, p.tiles_n, p.ksplit, p.kchunk, partial); break;
     case GEMM_RESIDUAL: launch_cfg<GEMM_RESIDUAL>(p.cfg, s, a, p.tiles_m, p.tiles_n, p.ksplit, p.kchunk, partial); break;
     default: launch_cfg<GEMM_SWIGLU>(p.cfg, s, a, p.tiles_m, p.tiles_n, p.ksplit, p.kchunk, partial); break;
+  }
+  if (p.ksplit > 1 && a.epi == GEMM_RESIDUAL && a.c_f32 && a.norm_out && a.N % 8 == 0 && a.ldc == a.N &&
+      a.N <= 8 * 256 * 8) {
+    const int nvec = a.N / 8;
+    if (nvec <= 256) splitk_reduce_rmsnorm_kernel<1><<<a.M, 256, 0, s>>>(a, p.ksplit, partial);
+    else if (nvec <= 1024) splitk_reduce_rmsnorm_kernel<4><<<a.M, 256, 0, s>>>(a, p.ksplit, partial);
+    else splitk_reduce_rmsnorm_kernel<8><<<a.M, 256, 0, s>>>(a, p.ksplit, partial);
+    return true;
   }
   if (p.ksplit > 1) {
     const int64_t items = a.epi == GEMM_QKV_ROPE
@@ -711,6 +810,7 @@ void launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& p, float* par
       default: splitk_reduce_kernel<GEMM_STORE_BF16><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
     }
   }
+  return false;
 }
 
 }  // namespace hb

@@ -248,7 +248,8 @@ def test_bf16_output_matches_fp32_output(hb):
 @pytest.mark.parametrize("ksplit", [1, 2, 3])
 def test_every_gemm_tile_shape(hb, monkeypatch, tile, ksplit):
     """Each LDS-pipelined GEMM tile shape, whole K or split (the split-K
-    reduce then applies RoPE + pool scatter, SwiGLU or the residual add),
+    reduce then applies RoPE + pool scatter, SwiGLU, or the residual add and,
+    after the O projection, the pre-FFN RMSNorm),
     through whole-layer parity and the q / SwiGLU stages; all four GEMMs here
     have K % 64 == 0 and ragged M and N tails."""
     from paper_2503_22562_amd import hb as H
@@ -266,5 +267,7 @@ def test_every_gemm_tile_shape(hb, monkeypatch, tile, ksplit):
     T = b.n_tokens
     q = oracle.bf16_bits_to_f64(bf16_bits(dl.stage(H.HB_STAGE_Q, T)))
     assert_stage(q, st["q"].reshape(T, -1), "q after RoPE")
+    h2 = dl.stage(H.HB_STAGE_H2, T).cpu().numpy()
+    assert_parity(h2, st["h2"], "h2")
     m = oracle.bf16_bits_to_f64(bf16_bits(dl.stage(H.HB_STAGE_MLP, T)))
     assert_stage(m, st["m"], "silu(gate)*up")
