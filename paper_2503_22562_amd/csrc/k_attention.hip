@@ -54,31 +54,50 @@ __device__ __forceinline__ void wait_vmcnt() {
 // 2^RESCALE_SLACK, which fp32 accumulation and bf16 weights carry without
 // loss. The result is exact either way (O, l and m change together), and the
 // O rescale -- a read-modify-write of every accumulator -- is mostly skipped.
-// Returns true when the accumulators must be scaled by alpha.
 constexpr float RESCALE_SLACK = 8.0f;
 
+// Common case: the weights against the current running maximum and their
+// sum. No cross-lane step maximum is needed: it returns (wave-uniform)
+// whether any weight's exponent exceeds the slack, and then the caller runs
+// softmax_rescale, which recomputes them.
 template <int N>
-__device__ __forceinline__ bool softmax_step(const float (&sv)[N], float sc, float& m, float& l, float& alpha,
-                                             float (&p)[N]) {
+__device__ __forceinline__ bool softmax_fast(const float (&sv)[N], float sc, float m, float& ps, float (&p)[N]) {
+  float t[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) t[i] = fmaf(sv[i], sc, -m);  // -inf for masked keys
+  float mx = t[0];
+#pragma unroll
+  for (int i = 1; i < N; ++i) mx = fmaxf(mx, t[i]);
+  const bool rescale = __any(mx > RESCALE_SLACK);
+  ps = 0.f;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    p[i] = __builtin_amdgcn_exp2f(t[i]);  // no denormal results needed
+    ps += p[i];
+  }
+  return rescale;
+}
+
+// Rare case: the column's exact step maximum (across the four lanes that
+// hold its keys) moves the running maximum; l is scaled by alpha (the caller
+// scales O) and the weights are recomputed.
+template <int N>
+__device__ __forceinline__ void softmax_rescale(const float (&sv)[N], float sc, float& m, float& l, float& alpha,
+                                                float& ps, float (&p)[N]) {
   float mx = sv[0];
 #pragma unroll
   for (int i = 1; i < N; ++i) mx = fmaxf(mx, sv[i]);
-  mx = rows_max(mx);
-  const float ms = mx * sc;  // -inf when every key of the step is masked
-  const bool rescale = __any(ms > m + RESCALE_SLACK);
-  // branch-free, so the caller's MFMAs can be scheduled across it
-  const float mn = rescale ? fmaxf(m, ms) : m;
-  alpha = __builtin_amdgcn_exp2f(m - mn);  // 1 without a rescale; 0 from the initial -1e30
+  const float ms = rows_max(mx) * sc;  // -inf when every key of the step is masked
+  const float mn = fmaxf(m, ms);
+  alpha = __builtin_amdgcn_exp2f(m - mn);  // 0 from the initial -1e30
   l *= alpha;
   m = mn;
-  float ps = 0.f;
+  ps = 0.f;
 #pragma unroll
   for (int i = 0; i < N; ++i) {
-    p[i] = __builtin_amdgcn_exp2f(fmaf(sv[i], sc, -m));  // no denormal results needed
+    p[i] = __builtin_amdgcn_exp2f(fmaf(sv[i], sc, -m));
     ps += p[i];
   }
-  l += ps;
-  return rescale;
 }
 
 // P^T operand of keys 32kk..32kk+31: slots 0..3 from block 2kk, 4..7 from 2kk+1.
@@ -172,9 +191,16 @@ __device__ __forceinline__ void wave_compute(const WaveStep<HD>& st, int j0, con
       for (int i = 0; i < 4; ++i)
         if (j0 + 16 * b + 4 * grp + i > lim) sv[4 * b + i] = -INFINITY;
   }
-  float alpha;
-  const bool rescale = softmax_step<8>(sv, sc, m, l, alpha, p);
-  const bf16x8 pf = p_operand(p, 0);
+  float ps;
+  bf16x8 pf;
+  if (softmax_fast<8>(sv, sc, m, ps, p)) {
+    float alpha;
+    softmax_rescale<8>(sv, sc, m, l, alpha, ps, p);
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) o[dt] *= alpha;
+  }
+  l += ps;
+  pf = p_operand(p, 0);
   // keys at or past kv_end may be unwritten slots holding non-finite bits
   // (0 * NaN would poison the sum): their V lanes are cleared
   uint32_t vm[2][2];
@@ -189,7 +215,6 @@ __device__ __forceinline__ void wave_compute(const WaveStep<HD>& st, int j0, con
     u32x2 v0 = st.v[0][dt], v1 = st.v[1][dt];
     v0[0] &= vm[0][0]; v0[1] &= vm[0][1];
     v1[0] &= vm[1][0]; v1[1] &= vm[1][1];
-    if (rescale) o[dt] *= alpha;
     o[dt] = mfma16x16x32(as_bf16x8(u32x4{v0[0], v0[1], v1[0], v1[1]}), pf, o[dt]);
   }
 }
@@ -268,12 +293,15 @@ struct TileGeom {
   static constexpr int KEYS_PER_LOAD = 1024 / ROW;
   static constexpr int CHUNKS = ROW / 16;        // 16-byte chunks per key row
   // A V block is four groups of four keys (HD * 8 bytes each). At HD 128 the
-  // groups sit 1152 bytes apart in LDS, so the two groups a half-wave reads
-  // together fall into different halves of the 64 banks.
-  static constexpr int VGS = HD == 128 ? HD * 8 + 128 : HD * 8;
-  static constexpr int VBLK = 4 * VGS;
-  static constexpr int V_LOAD_STRIDE = HD == 128 ? VGS : 1024;  // LDS distance of consecutive 1-KB V loads
-  static constexpr int STAGE = 2 * BLK + 2 * VBLK;  // 2 K blocks then 2 V blocks
+  // same group of the step's two blocks sits side by side (1 KB apart) and
+  // groups are 2176 bytes apart, so the two groups a half-wave reads together
+  // fall into different halves of the 64 banks. At HD 64 the blocks follow
+  // each other (four 512-byte groups each).
+  static constexpr int VGS = HD == 128 ? 2 * HD * 8 + 128 : HD * 8;  // LDS distance of groups
+  static constexpr int VBLK = HD == 128 ? HD * 8 : 4 * VGS;          // LDS distance of the two blocks
+  static constexpr int V_LOAD_STRIDE = HD == 128 ? VGS : 1024;      // LDS distance of consecutive 1-KB V loads
+  static constexpr int V_BYTES = HD == 128 ? 4 * VGS : 2 * VBLK;    // LDS bytes of the step's V
+  static constexpr int STAGE = 2 * BLK + V_BYTES;  // 2 K blocks then the V of both
   // 16-byte chunk c of K row r is stored at chunk c ^ kswz(r): the 16 rows a
   // fragment read touches then cover all bank positions
   static constexpr __host__ __device__ int kswz(int r) { return HD == 128 ? (r & 15) : ((r >> 1) & 7); }
@@ -321,28 +349,36 @@ __device__ __forceinline__ void tile_read_k(bf16x8 (&kf)[2][HD / 32], const uint
       kf[b][kc] = as_bf16x8(*reinterpret_cast<const u32x4*>(st + b * TG::BLK + k_lane + (((4 * kc + grp) ^ TG::kswz(col)) << 4)));
 }
 
-// MASKED: the V lanes of keys past kv_end are cleared (unwritten slots may
-// hold non-finite bits, and 0 * NaN would poison the sum).
-template <int HD, bool MASKED>
-__device__ __forceinline__ void tile_read_v(u32x4 (&vf)[HD / 16], const uint8_t* st, int v_lane, int j0, int kv_end,
-                                            int grp) {
+// V^T fragments of one step: keys 4 grp..+3 of both blocks for dims
+// 16 dt + col.
+template <int HD>
+__device__ __forceinline__ void tile_read_v(u32x4 (&vf)[HD / 16], const uint8_t* st, int v_lane) {
   using TG = TileGeom<HD>;
   const uint8_t* vs = st + 2 * TG::BLK + v_lane;
-  uint32_t vm[4] = {~0u, ~0u, ~0u, ~0u};
-  if (MASKED) {
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int k0 = j0 + 16 * b + 4 * grp;
-      vm[2 * b] = (k0 < kv_end ? 0xFFFFu : 0u) | (k0 + 1 < kv_end ? 0xFFFF0000u : 0u);
-      vm[2 * b + 1] = (k0 + 2 < kv_end ? 0xFFFFu : 0u) | (k0 + 3 < kv_end ? 0xFFFF0000u : 0u);
-    }
-  }
 #pragma unroll
   for (int dt = 0; dt < HD / 16; ++dt) {
     const u32x2 va = *reinterpret_cast<const u32x2*>(vs + dt * 128);
     const u32x2 vb = *reinterpret_cast<const u32x2*>(vs + TG::VBLK + dt * 128);
-    vf[dt] = u32x4{va[0] & vm[0], va[1] & vm[1], vb[0] & vm[2], vb[1] & vm[3]};
+    vf[dt] = u32x4{va[0], va[1], vb[0], vb[1]};
   }
+}
+
+// MASKED: the V lanes of keys past kv_end are cleared (unwritten slots may
+// hold non-finite bits, and 0 * NaN would poison the sum).
+template <int HD, bool MASKED>
+__device__ __forceinline__ void tile_mask_v(u32x4 (&vf)[HD / 16], int j0, int kv_end, int grp) {
+  if (!MASKED) return;
+  uint32_t vm[4];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int k0 = j0 + 16 * b + 4 * grp;
+    vm[2 * b] = (k0 < kv_end ? 0xFFFFu : 0u) | (k0 + 1 < kv_end ? 0xFFFF0000u : 0u);
+    vm[2 * b + 1] = (k0 + 2 < kv_end ? 0xFFFFu : 0u) | (k0 + 3 < kv_end ? 0xFFFF0000u : 0u);
+  }
+#pragma unroll
+  for (int dt = 0; dt < HD / 16; ++dt)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) vf[dt][e] &= vm[e];
 }
 
 template <int HD, int CT>
@@ -358,30 +394,31 @@ __device__ __forceinline__ void tile_scores(f32x4 (&sc)[CT][2], const bf16x8 (&k
     }
 }
 
-// Online softmax of one step for the wave's CT column tiles, branch-free.
-// MASKED: keys past a column's position or past kv_end get no weight.
+// Online softmax of one step for the wave's CT column tiles: the common
+// case (branch-free, so the score MFMAs can be scheduled across it) gives
+// the weights pf and their sums ps against the running maxima; it returns
+// whether tile_rescale must run. MASKED: keys past a column's position or
+// past kv_end get no weight.
 template <int HD, int CT, bool MASKED>
-__device__ __forceinline__ bool tile_softmax(const f32x4 (&sc)[CT][2], bf16x8 (&pf)[CT], float (&m)[CT],
-                                             float (&l)[CT], float (&alpha)[CT], const int (&pos)[CT], int j0,
+__device__ __forceinline__ bool tile_softmax(const f32x4 (&sc)[CT][2], float (&sv)[CT][8], float (&p)[CT][8],
+                                             float (&ps)[CT], const float (&m)[CT], const int (&pos)[CT], int j0,
                                              int kv_end, int grp, float scale) {
   bool rescale = false;
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct) {
-    float sv[8], p[8];
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) sv[4 * b + i] = sc[ct][b][i];
+      for (int i = 0; i < 4; ++i) sv[ct][4 * b + i] = sc[ct][b][i];
     if (MASKED) {
       const int lim = min(pos[ct], kv_end - 1);
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if (j0 + 16 * b + 4 * grp + i > lim) sv[4 * b + i] = -INFINITY;
+          if (j0 + 16 * b + 4 * grp + i > lim) sv[ct][4 * b + i] = -INFINITY;
     }
-    rescale |= softmax_step<8>(sv, scale, m[ct], l[ct], alpha[ct], p);
-    pf[ct] = p_operand(p, 0);
+    rescale |= softmax_fast<8>(sv[ct], scale, m[ct], ps[ct], p[ct]);
   }
   return rescale;
 }
@@ -408,7 +445,7 @@ __device__ __forceinline__ void tile_step(const AttnArgs& a, const AttnItem& it,
   // V fragments of this step (their LDS latency hides under the score MFMAs)
   const int j0 = it.kv_begin + TSTEP * kt;
   u32x4 vf[HD / 16];
-  tile_read_v<HD, MASKED>(vf, smem + (kt % TSTAGES) * TG::STAGE, v_lane, j0, it.kv_end, grp);
+  tile_read_v<HD>(vf, smem + (kt % TSTAGES) * TG::STAGE, v_lane);
   if (!LAST) {
     // step kt + 1 complete (the one issued after it may stay in flight); the
     // ring slot of step kt - 1 is free for step kt + TSTAGES - 1
@@ -423,9 +460,11 @@ __device__ __forceinline__ void tile_step(const AttnArgs& a, const AttnItem& it,
     tile_read_k<HD>(kf, smem + ((kt + 1) % TSTAGES) * TG::STAGE, k_lane, grp, col);
     tile_scores<HD, CT>(sc_next, kf, qf);
   }
+  float sv[CT][8], p[CT][8], ps[CT];
+  const bool rescale = tile_softmax<HD, CT, MASKED>(sc_cur, sv, p, ps, m, pos, j0, it.kv_end, grp, a.scale_log2);
   bf16x8 pf[CT];
-  float alpha[CT];
-  const bool rescale = tile_softmax<HD, CT, MASKED>(sc_cur, pf, m, l, alpha, pos, j0, it.kv_end, grp, a.scale_log2);
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct) pf[ct] = p_operand(p[ct], 0);
   // keep the weights' computation here, under the score MFMAs, rather than
   // letting it sink past the rescale branch into the PV block
 #pragma unroll
@@ -437,10 +476,17 @@ __device__ __forceinline__ void tile_step(const AttnArgs& a, const AttnItem& it,
   __builtin_amdgcn_sched_barrier(0);
   if (rescale) {
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
+    for (int ct = 0; ct < CT; ++ct) {
+      float alpha;
+      softmax_rescale<8>(sv[ct], a.scale_log2, m[ct], l[ct], alpha, ps[ct], p[ct]);
+      pf[ct] = p_operand(p[ct], 0);
 #pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) o[ct][dt] *= alpha[ct];
+      for (int dt = 0; dt < HD / 16; ++dt) o[ct][dt] *= alpha;
+    }
   }
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct) l[ct] += ps[ct];
+  tile_mask_v<HD, MASKED>(vf, j0, it.kv_end, grp);
   tile_pv<HD, CT>(o, vf, pf);
 }
 
