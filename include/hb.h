@@ -80,10 +80,11 @@ typedef struct {
 
 /* Paged KV cache of one layer: device bf16, caller-owned.
  *   k_pool  [num_blocks][n_kv_heads][16][head_dim]        K of slot s at [..][s][d]
- *   v_pool  [num_blocks][n_kv_heads][4][head_dim][4]      V of slot s at [..][s/4][d][s%4]
+ *   v_pool  [num_blocks][n_kv_heads][2][head_dim][8]      V of slot s at [..][s/8][d][s%8]
  * Position p of a request lives in block block_table[p / 16], slot p % 16.
- * Keys are stored after RoPE. Within a block, V is grouped by four slots and
- * is dimension-major inside a group, the operand order of the PV product. */
+ * Keys are stored after RoPE. Within a block, V is split into two halves of
+ * eight slots, dimension-major inside a half: the eight keys of one dimension
+ * are one 16-byte operand of the PV product. */
 typedef struct {
   void *k_pool, *v_pool;
   int32_t num_blocks;

@@ -143,11 +143,16 @@ __device__ __forceinline__ void store_column(const AttnArgs& a, const AttnItem& 
 
 // ---------------------------------------------------------------------------
 // wave item: 16 columns, K/V streamed into registers, one step ahead
+//
+// Key order of a 32-key step (both pool blocks): score MFMA b takes, in its
+// row r, key 8 (r / 4) + 4 b + r % 4, so the lanes of row group g end up with
+// the scores of keys 8 g .. 8 g + 7 -- the eight keys one lane feeds to the
+// PV MFMA, stored together (16 bytes) in the V pool.
 // ---------------------------------------------------------------------------
 template <int HD>
 struct WaveStep {
-  u32x4 k[2][HD / 32];  // per block: the lane's key row, 8 dims of each 32-dim chunk
-  u32x2 v[2][HD / 16];  // per block: 4 keys of one dim per 16-dim tile
+  u32x4 k[2][HD / 32];  // per score MFMA: the lane's key row, 8 dims of each 32-dim chunk
+  u32x4 v[HD / 16];     // per 16-dim tile: keys 8 grp..+7 of one dim
 };
 
 template <int HD>
@@ -155,16 +160,31 @@ __device__ __forceinline__ void wave_load(WaveStep<HD>& st, const AttnArgs& a, i
                                           int grp) {
   const size_t blk_stride = (size_t)a.nkv * 16 * HD;
   const size_t head_off = (size_t)g * 16 * HD;
+  // K: this lane's rows (keys 8 (col / 4) + 4 b + col % 4) lie in block col / 8
+  const uint16_t* K = a.k_pool + (size_t)((col >> 3) ? id1 : id0) * blk_stride + head_off +
+                      (8 * ((col >> 2) & 1) + (col & 3)) * HD + 8 * grp;
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int id = b ? id1 : id0;
-    const uint16_t* K = a.k_pool + (size_t)id * blk_stride + head_off;
-    const uint16_t* V = a.v_pool + (size_t)id * blk_stride + head_off;
+  for (int b = 0; b < 2; ++b)
 #pragma unroll
-    for (int kc = 0; kc < HD / 32; ++kc) st.k[b][kc] = ld16(K + col * HD + 32 * kc + 8 * grp);
+    for (int kc = 0; kc < HD / 32; ++kc) st.k[b][kc] = ld16(K + 4 * b * HD + 32 * kc);
+  // V: keys 8 grp..+7 are half grp % 2 of block grp / 2
+  const uint16_t* V = a.v_pool + (size_t)((grp >> 1) ? id1 : id0) * blk_stride + head_off +
+                      ((grp & 1) * HD + col) * 8;
 #pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt) st.v[b][dt] = ld8(V + (grp * HD + 16 * dt + col) * 4);
+  for (int dt = 0; dt < HD / 16; ++dt) st.v[dt] = ld16(V + 16 * dt * 8);
+}
+
+// Lane mask of the eight keys j0 + 8 grp .. +7 of a V^T operand: keys at or
+// past kv_end may be unwritten slots holding non-finite bits (0 * NaN would
+// poison the sum), so their bf16 lanes are cleared.
+__device__ __forceinline__ u32x4 v_key_mask(int j0, int kv_end, int grp) {
+  u32x4 vm;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const int k = j0 + 8 * grp + 2 * w;
+    vm[w] = (k < kv_end ? 0xFFFFu : 0u) | (k + 1 < kv_end ? 0xFFFF0000u : 0u);
   }
+  return vm;
 }
 
 template <int HD>
@@ -189,7 +209,7 @@ __device__ __forceinline__ void wave_compute(const WaveStep<HD>& st, int j0, con
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        if (j0 + 16 * b + 4 * grp + i > lim) sv[4 * b + i] = -INFINITY;
+        if (j0 + 8 * grp + 4 * b + i > lim) sv[4 * b + i] = -INFINITY;
   }
   float ps;
   bf16x8 pf;
@@ -201,21 +221,13 @@ __device__ __forceinline__ void wave_compute(const WaveStep<HD>& st, int j0, con
   }
   l += ps;
   pf = p_operand(p, 0);
-  // keys at or past kv_end may be unwritten slots holding non-finite bits
-  // (0 * NaN would poison the sum): their V lanes are cleared
-  uint32_t vm[2][2];
+  if (j0 + WSTEP > it.kv_end) {  // tail step (wave-uniform)
+    const u32x4 vm = v_key_mask(j0, it.kv_end, grp);
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int k0 = j0 + 16 * b + 4 * grp;
-    vm[b][0] = (k0 < it.kv_end ? 0xFFFFu : 0u) | (k0 + 1 < it.kv_end ? 0xFFFF0000u : 0u);
-    vm[b][1] = (k0 + 2 < it.kv_end ? 0xFFFFu : 0u) | (k0 + 3 < it.kv_end ? 0xFFFF0000u : 0u);
-  }
+    for (int dt = 0; dt < HD / 16; ++dt) o[dt] = mfma16x16x32(as_bf16x8(st.v[dt] & vm), pf, o[dt]);
+  } else {
 #pragma unroll
-  for (int dt = 0; dt < HD / 16; ++dt) {
-    u32x2 v0 = st.v[0][dt], v1 = st.v[1][dt];
-    v0[0] &= vm[0][0]; v0[1] &= vm[0][1];
-    v1[0] &= vm[1][0]; v1[1] &= vm[1][1];
-    o[dt] = mfma16x16x32(as_bf16x8(u32x4{v0[0], v0[1], v1[0], v1[1]}), pf, o[dt]);
+    for (int dt = 0; dt < HD / 16; ++dt) o[dt] = mfma16x16x32(as_bf16x8(st.v[dt]), pf, o[dt]);
   }
 }
 
@@ -287,28 +299,25 @@ constexpr int TSTAGES = 4;   // LDS ring depth of the tile path
 
 template <int HD>
 struct TileGeom {
-  static constexpr int BLK = 16 * HD * 2;        // bytes of one K block of one head
+  static constexpr int BLK = 16 * HD * 2;        // bytes of one K (or V) block of one head
   static constexpr int ROW = HD * 2;             // bytes of one key row
   static constexpr int LOADS = BLK / 1024;       // 1-KB loads per block
   static constexpr int KEYS_PER_LOAD = 1024 / ROW;
   static constexpr int CHUNKS = ROW / 16;        // 16-byte chunks per key row
-  // A V block is four groups of four keys (HD * 8 bytes each). At HD 128 the
-  // same group of the step's two blocks sits side by side (1 KB apart) and
-  // groups are 2176 bytes apart, so the two groups a half-wave reads together
-  // fall into different halves of the 64 banks. At HD 64 the blocks follow
-  // each other (four 512-byte groups each).
-  static constexpr int VGS = HD == 128 ? 2 * HD * 8 + 128 : HD * 8;  // LDS distance of groups
-  static constexpr int VBLK = HD == 128 ? HD * 8 : 4 * VGS;          // LDS distance of the two blocks
-  static constexpr int V_LOAD_STRIDE = HD == 128 ? VGS : 1024;      // LDS distance of consecutive 1-KB V loads
-  static constexpr int V_BYTES = HD == 128 ? 4 * VGS : 2 * VBLK;    // LDS bytes of the step's V
-  static constexpr int STAGE = 2 * BLK + V_BYTES;  // 2 K blocks then the V of both
-  // 16-byte chunk c of K row r is stored at chunk c ^ kswz(r): the 16 rows a
-  // fragment read touches then cover all bank positions
-  static constexpr __host__ __device__ int kswz(int r) { return HD == 128 ? (r & 15) : ((r >> 1) & 7); }
+  // Both V blocks are copied as stored ([half][dim][8 keys] each), so the
+  // 16 bytes of keys 8 g..8 g+7 of dim d sit at g * HD * 16 + d * 16.
+  static constexpr int STAGE = 4 * BLK;  // 2 K blocks then 2 V blocks
+  // 16-byte chunk c of K row r of block b is stored at chunk c ^ kswz(b, r).
+  // The 16 rows one fragment read touches (rows 0-3 and 8-11, or 4-7 and
+  // 12-15, of both blocks) then cover all bank positions; rows r and r + 4
+  // share the pattern, so the two score MFMAs' reads differ by a constant.
+  static constexpr __host__ __device__ int kswz(int b, int r) {
+    return HD == 128 ? ((r & 11) ^ (b << 2)) : (((r >> 1) & 1) | (((r >> 3) & 1) << 1) | (b << 2));
+  }
 };
 
 // One step is four blocks in the stage: K of the two pool blocks (rows
-// chunk-swizzled), then their V (groups spaced by VGS). Wave b copies stage
+// chunk-swizzled), then their V. Wave b copies stage
 // block b: the K (b = 0, 1) or V (b = 2, 3) of pool block b & 1.
 template <int HD>
 __device__ __forceinline__ void tile_issue(uint8_t* stage, const AttnArgs& a, int id, int g, int wave, int lane) {
@@ -323,62 +332,50 @@ __device__ __forceinline__ void tile_issue(uint8_t* stage, const AttnArgs& a, in
 #pragma unroll
     for (int i = 0; i < TG::LOADS; ++i) {
       const int kk = i * TG::KEYS_PER_LOAD + kk_lane;
-      const uint16_t* src = K + kk * HD + 8 * (pc ^ TG::kswz(kk));
+      const uint16_t* src = K + kk * HD + 8 * (pc ^ TG::kswz(b, kk));
       __builtin_amdgcn_global_load_lds(src, dst + i * 1024, 16, 0, 0);
     }
   } else {
-    uint8_t* dst = stage + 2 * TG::BLK + (b - 2) * TG::VBLK;
+    uint8_t* dst = stage + 2 * TG::BLK + (b - 2) * TG::BLK;
     const uint8_t* V = reinterpret_cast<const uint8_t*>(a.v_pool + off);
 #pragma unroll
     for (int i = 0; i < TG::LOADS; ++i) {
-      uint8_t* d = dst + i * TG::V_LOAD_STRIDE;
+      uint8_t* d = dst + i * 1024;
       __builtin_amdgcn_global_load_lds(V + i * 1024 + lane * 16, d, 16, 0, 0);
     }
   }
 }
 
-// Fragments of one step from a stage: K^T rows of both pool blocks (swizzled
-// chunks), and the V^T fragments (keys 4 grp..+3 of both blocks).
+// Fragments of one step from a stage. K: for score MFMA b, the lane's key
+// row, at k_lane (block and row of key 8 (col / 4) + col % 4, OR-ed with the
+// lane's swizzled chunk (grp ^ kswz) * 16; 4 rows further for b = 1; chunk
+// 4 kc + grp is the XOR with kc * 64). V: keys 8 grp..+7 of dims 16 dt + col
+// (v_lane = grp * HD * 16 + col * 16).
 template <int HD>
-__device__ __forceinline__ void tile_read_k(bf16x8 (&kf)[2][HD / 32], const uint8_t* st, int k_lane, int grp, int col) {
+__device__ __forceinline__ void tile_read_k(bf16x8 (&kf)[2][HD / 32], const uint8_t* st, int k_lane) {
   using TG = TileGeom<HD>;
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
     for (int kc = 0; kc < HD / 32; ++kc)
-      kf[b][kc] = as_bf16x8(*reinterpret_cast<const u32x4*>(st + b * TG::BLK + k_lane + (((4 * kc + grp) ^ TG::kswz(col)) << 4)));
+      kf[b][kc] = as_bf16x8(*reinterpret_cast<const u32x4*>(st + 4 * b * TG::ROW + (k_lane ^ (kc << 6))));
 }
 
-// V^T fragments of one step: keys 4 grp..+3 of both blocks for dims
-// 16 dt + col.
 template <int HD>
 __device__ __forceinline__ void tile_read_v(u32x4 (&vf)[HD / 16], const uint8_t* st, int v_lane) {
   using TG = TileGeom<HD>;
   const uint8_t* vs = st + 2 * TG::BLK + v_lane;
 #pragma unroll
-  for (int dt = 0; dt < HD / 16; ++dt) {
-    const u32x2 va = *reinterpret_cast<const u32x2*>(vs + dt * 128);
-    const u32x2 vb = *reinterpret_cast<const u32x2*>(vs + TG::VBLK + dt * 128);
-    vf[dt] = u32x4{va[0], va[1], vb[0], vb[1]};
-  }
+  for (int dt = 0; dt < HD / 16; ++dt) vf[dt] = *reinterpret_cast<const u32x4*>(vs + dt * 256);
 }
 
-// MASKED: the V lanes of keys past kv_end are cleared (unwritten slots may
-// hold non-finite bits, and 0 * NaN would poison the sum).
+// MASKED: the V lanes of keys past kv_end are cleared.
 template <int HD, bool MASKED>
 __device__ __forceinline__ void tile_mask_v(u32x4 (&vf)[HD / 16], int j0, int kv_end, int grp) {
   if (!MASKED) return;
-  uint32_t vm[4];
+  const u32x4 vm = v_key_mask(j0, kv_end, grp);
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int k0 = j0 + 16 * b + 4 * grp;
-    vm[2 * b] = (k0 < kv_end ? 0xFFFFu : 0u) | (k0 + 1 < kv_end ? 0xFFFF0000u : 0u);
-    vm[2 * b + 1] = (k0 + 2 < kv_end ? 0xFFFFu : 0u) | (k0 + 3 < kv_end ? 0xFFFF0000u : 0u);
-  }
-#pragma unroll
-  for (int dt = 0; dt < HD / 16; ++dt)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) vf[dt][e] &= vm[e];
+  for (int dt = 0; dt < HD / 16; ++dt) vf[dt] &= vm;
 }
 
 template <int HD, int CT>
@@ -416,7 +413,7 @@ __device__ __forceinline__ bool tile_softmax(const f32x4 (&sc)[CT][2], float (&s
       for (int b = 0; b < 2; ++b)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if (j0 + 16 * b + 4 * grp + i > lim) sv[ct][4 * b + i] = -INFINITY;
+          if (j0 + 8 * grp + 4 * b + i > lim) sv[ct][4 * b + i] = -INFINITY;
     }
     rescale |= softmax_fast<8>(sv[ct], scale, m[ct], ps[ct], p[ct]);
   }
@@ -457,7 +454,7 @@ __device__ __forceinline__ void tile_step(const AttnArgs& a, const AttnItem& it,
       if (kt + TSTAGES < nsteps) next_id = const_load(btab + min(kb0 + 2 * (kt + TSTAGES) + (wave & 1), kb_last));
     }
     bf16x8 kf[2][HD / 32];
-    tile_read_k<HD>(kf, smem + ((kt + 1) % TSTAGES) * TG::STAGE, k_lane, grp, col);
+    tile_read_k<HD>(kf, smem + ((kt + 1) % TSTAGES) * TG::STAGE, k_lane);
     tile_scores<HD, CT>(sc_next, kf, qf);
   }
   float sv[CT][8], p[CT][8], ps[CT];
@@ -531,8 +528,9 @@ __device__ __forceinline__ void tile_unit(const AttnArgs& a, const AttnItem& it,
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct) { m[ct] = NEG_BIG; l[ct] = 0.f; }
 
-  const int k_lane = col * TG::ROW;
-  const int v_lane = grp * TG::VGS + col * 8;
+  const int k_row = 8 * ((col >> 2) & 1) + (col & 3);  // row of key 8 (col / 4) + col % 4 in block col / 8
+  const int k_lane = (col >> 3) * TG::BLK + k_row * TG::ROW + ((grp ^ TG::kswz(col >> 3, k_row)) << 4);
+  const int v_lane = grp * HD * 16 + col * 16;
   // prologue: steps 0..TSTAGES-2 in flight, scores of step 0
   int next_id = const_load(btab + min(kb0 + (wave & 1), kb_last));
 #pragma unroll
@@ -547,7 +545,7 @@ __device__ __forceinline__ void tile_unit(const AttnArgs& a, const AttnItem& it,
   f32x4 sa[CT][2], sb[CT][2];
   {
     bf16x8 kf[2][KC];
-    tile_read_k<HD>(kf, smem, k_lane, grp, col);
+    tile_read_k<HD>(kf, smem, k_lane);
     tile_scores<HD, CT>(sa, kf, qf);
   }
   // steps alternate the two score buffers; the last step is peeled

@@ -310,9 +310,9 @@ __device__ __forceinline__ void qkv_rope_row(const GemmArgs& a, const f32x4 (&ac
       st8(dst + HALF + j, wh);
     } else {
       const int g = (n - qk_end) / HD, d = n % HD;
-      uint16_t* vp = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * HD + ((slot >> 2) * HD + d) * 4 + (slot & 3);
+      uint16_t* vp = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * HD + ((slot >> 3) * HD + d) * 8 + (slot & 7);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) vp[4 * e] = (uint16_t)f32_to_bf16(acc[ni][e]);
+      for (int e = 0; e < 4; ++e) vp[8 * e] = (uint16_t)f32_to_bf16(acc[ni][e]);
     }
   }
 }
@@ -568,8 +568,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int kspl
         r -= qk_units;
         const int g = r / (hd / 4), d = (r - g * (hd / 4)) * 4;
         const f32x4 c = sum4(m, (qk_heads + g) * hd + d);
-        uint16_t* vp = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * hd + ((slot >> 2) * hd + d) * 4 + (slot & 3);
-        for (int e = 0; e < 4; ++e) vp[4 * e] = (uint16_t)f32_to_bf16(c[e]);
+        uint16_t* vp = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * hd + ((slot >> 3) * hd + d) * 8 + (slot & 7);
+        for (int e = 0; e < 4; ++e) vp[8 * e] = (uint16_t)f32_to_bf16(c[e]);
       }
     }
     return;

@@ -27,7 +27,7 @@ def to_device_bf16(bits: np.ndarray, device: str = "cuda"):
 
 
 def v_by_slot(v_bits: np.ndarray) -> np.ndarray:
-    """View a V pool [blocks][kv][4][hd][4] as [blocks][kv][slot][hd]."""
+    """View a V pool [blocks][kv][2][hd][8] as [blocks][kv][slot][hd]."""
     nb, nkv, _, hd, _ = v_bits.shape
     return v_bits.transpose(0, 1, 2, 4, 3).reshape(nb, nkv, 16, hd)
 
@@ -65,7 +65,7 @@ class DeviceLayer:
         self.w = {n: to_device_bf16(weights_bits[n], device) for n in WEIGHT_NAMES}
         nkv, hd = shape.n_kv_heads, shape.head_dim
         self.k_pool = torch.empty((num_blocks, nkv, 16, hd), dtype=torch.bfloat16, device=device)
-        self.v_pool = torch.empty((num_blocks, nkv, 4, hd, 4), dtype=torch.bfloat16, device=device)
+        self.v_pool = torch.empty((num_blocks, nkv, 2, hd, 8), dtype=torch.bfloat16, device=device)
         if pool_fill_bits is not None:
             fill = int(np.array([pool_fill_bits], dtype=np.uint16).view(np.int16)[0])
             self.k_pool.view(torch.int16).fill_(fill)
