@@ -166,12 +166,12 @@ __device__ __forceinline__ void wave_load(WaveStep<HD>& st, const AttnArgs& a, i
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
-    for (int kc = 0; kc < HD / 32; ++kc) st.k[b][kc] = ld16(K + 4 * b * HD + 32 * kc);
+    for (int kc = 0; kc < HD / 32; ++kc) st.k[b][kc] = ld16_stream(K + 4 * b * HD + 32 * kc);
   // V: keys 8 grp..+7 are half grp % 2 of block grp / 2
   const uint16_t* V = a.v_pool + (size_t)((grp >> 1) ? id1 : id0) * blk_stride + head_off +
                       ((grp & 1) * HD + col) * 8;
 #pragma unroll
-  for (int dt = 0; dt < HD / 16; ++dt) st.v[dt] = ld16(V + 16 * dt * 8);
+  for (int dt = 0; dt < HD / 16; ++dt) st.v[dt] = ld16_stream(V + 16 * dt * 8);
 }
 
 // Lane mask of the eight keys j0 + 8 grp .. +7 of a V^T operand: keys at or
