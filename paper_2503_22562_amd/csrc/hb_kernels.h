@@ -28,6 +28,11 @@ void launch_rmsnorm(hipStream_t s, const void* x, bool x_f32, const uint16_t* g,
 
 enum GemmEpilogue { GEMM_STORE_BF16 = 0, GEMM_RESIDUAL = 1, GEMM_SWIGLU = 2, GEMM_QKV_ROPE = 3 };
 
+// Rows past M that a GEMM's A operand must keep readable: the LDS-pipelined
+// kernels load whole row tiles (at most 288 rows) and never store the rows
+// past M. Their B operands need N % 8 == 0 (8-row load groups).
+constexpr int kGemmPadRows = 512;
+
 // C[M][N] = A[M][K] * B[N][K]^T with an epilogue:
 //   GEMM_STORE_BF16: C bf16
 //   GEMM_RESIDUAL:   C = R + A B^T, R bf16 or fp32, C fp32 or bf16

@@ -364,11 +364,12 @@ hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w,
   if (const char* e = std::getenv("HB_ATTN_SPLIT_ITEM")) L->plan_opt.split_item = std::atoi(e);
   if (const char* e = std::getenv("HB_ATTN_UNIT_BLOCK")) L->plan_opt.unit_block = std::atoi(e);
   const size_t T = d.max_T;
+  const size_t TA = T + kGemmPadRows;  // GEMM A operands: rows past M stay readable
   struct Alloc { void** p; size_t bytes; } allocs[] = {
-      {(void**)&L->xn, T * d.H * 2},         {(void**)&L->rope_cs, T * d.hd * 4},
+      {(void**)&L->xn, TA * d.H * 2},        {(void**)&L->rope_cs, T * d.hd * 4},
       {(void**)&L->tok_slot, T * 4},
-      {(void**)&L->q_rot, T * d.nq * d.hd * 2}, {(void**)&L->attn, T * d.nq * d.hd * 2},
-      {(void**)&L->mlp, T * d.F * 2},        {(void**)&L->h2, T * d.H * 4},
+      {(void**)&L->q_rot, T * d.nq * d.hd * 2}, {(void**)&L->attn, TA * d.nq * d.hd * 2},
+      {(void**)&L->mlp, TA * d.F * 2},       {(void**)&L->h2, T * d.H * 4},
       {(void**)&L->inv_freq, (size_t)d.hd / 2 * sizeof(double)},
   };
   for (auto& a : allocs)

@@ -191,19 +191,36 @@ __device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0
 
 // One K stage (64 columns) of the A and B tiles: LA (LB) 1-KB loads fill the
 // A (B) tile, 8 rows each; wave w issues loads w, w + NW, w + 2 NW, ...
-// (NA / NB slots, the last possibly empty); lane L of a load lands at byte 16 L.
-template <int NW, int LA, int LB>
-__device__ __forceinline__ void issue_stage(uint8_t* base, int a_bytes, const uint16_t* Abase, const uint16_t* Bbase,
-                                            const uint32_t* aoff, const uint32_t* boff, int wave, int koff) {
-  constexpr int NA = (LA + NW - 1) / NW, NB = (LB + NW - 1) / NW;
+// (NA / NB slots, the last possibly empty); lane L of a load lands at byte
+// 16 L. The loads are buffer loads straight into LDS: the wave-uniform byte
+// offset of each slot's 8-row group (ao / bo, plus the stage's K offset) is a
+// scalar operand, and the lane's offset inside the group (la / lb) the only
+// vector one, so no per-load address registers are needed.
+template <int NW, int LA, int LB, int NA, int NB>
+__device__ __forceinline__ void issue_stage(uint8_t* base, int a_bytes, __amdgpu_buffer_rsrc_t ra,
+                                            __amdgpu_buffer_rsrc_t rb, const uint32_t (&ao)[NA],
+                                            const uint32_t (&bo)[NB], uint32_t la, uint32_t lb, int wave,
+                                            uint32_t kbytes) {
+  typedef __attribute__((address_space(3))) void* lds_ptr;
 #pragma unroll
   for (int j = 0; j < NA; ++j)
-    if (LA % NW == 0 || j * NW + wave < LA)
-      __builtin_amdgcn_global_load_lds(Abase + aoff[j] + koff, base + (j * NW + wave) * 1024, 16, 0, 0);
+    if (LA % NW == 0 || j * NW + wave < LA) {
+      uint8_t* p = base + (j * NW + wave) * 1024;
+      const uint32_t so = ao[j] + kbytes;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)p, 16, la, so, 0, 0);
+    }
 #pragma unroll
   for (int j = 0; j < NB; ++j)
-    if (LB % NW == 0 || j * NW + wave < LB)
-      __builtin_amdgcn_global_load_lds(Bbase + boff[j] + koff, base + a_bytes + (j * NW + wave) * 1024, 16, 0, 0);
+    if (LB % NW == 0 || j * NW + wave < LB) {
+      uint8_t* p = base + a_bytes + (j * NW + wave) * 1024;
+      const uint32_t so = bo[j] + kbytes;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)p, 16, lb, so, 0, 0);
+    }
+}
+
+// Buffer resource over [p, p + bytes) for raw (unstrided) loads.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
 }
 
 // Fragment reads of one K half: TM A fragments (16-row blocks 2 KB apart)
@@ -346,30 +363,30 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
   const int k_end = min(a.K, k_begin + kchunk);
   const int nk = (k_end - k_begin) >> 6;
 
-  // per-lane source offsets (elements) of this wave's load slots, rows
-  // clamped in range: rows past M or N only feed outputs never stored
+  // Load offsets (bytes): the first row of each of this wave's 8-row groups
+  // is wave-uniform; a lane adds row lrow and its swizzled 16-byte chunk.
+  // A rows past M read the caller's padding rows (they only feed outputs that
+  // are never stored); B row groups past N are clamped whole (N % 8 == 0).
   const int lrow = lane >> 3;
   const int lchunk = (lane & 7) ^ lrow;
-  uint32_t aoff[NA], boff[NB];
+  const uint32_t la = 2u * (uint32_t)(lrow * a.lda + 8 * lchunk), lb = 2u * (uint32_t)(lrow * a.ldb + 8 * lchunk);
+  uint32_t ao[NA], bo[NB];
 #pragma unroll
-  for (int j = 0; j < NA; ++j) {
-    const int row = min(8 * (j * NW + wave) + lrow, BM - 1);
-    aoff[j] = (uint32_t)min(m0 + row, M - 1) * (uint32_t)a.lda + 8 * lchunk;
-  }
+  for (int j = 0; j < NA; ++j) ao[j] = 2u * (uint32_t)(m0 + min(8 * (j * NW + wave), BM - 8)) * (uint32_t)a.lda;
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
-    const int row = min(8 * (j * NW + wave) + lrow, BN - 1);
+    const int r8 = min(8 * (j * NW + wave), BN - 8);
     int brow;
     if (EPI == GEMM_SWIGLU) {
-      const int c = min(nt * (BN / 2) + (row % (BN / 2)), N - 1);
-      brow = (row < BN / 2) ? c : N + c;
+      const int c = min(nt * (BN / 2) + (r8 % (BN / 2)), N - 8);
+      brow = (r8 < BN / 2) ? c : N + c;
     } else {
-      brow = min(nt * BN + row, N - 1);
+      brow = min(nt * BN + r8, N - 8);
     }
-    boff[j] = (uint32_t)brow * (uint32_t)a.ldb + 8 * lchunk;
+    bo[j] = 2u * (uint32_t)brow * (uint32_t)a.ldb;
   }
-  const uint16_t* Abase = a.A + k_begin;
-  const uint16_t* Bbase = a.B + k_begin;
+  const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(a.A + k_begin, 0x7FFFFFF0u);
+  const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(a.B + k_begin, 0x7FFFFFF0u);
 
   f32x4 acc[TM][TN];
 #pragma unroll
@@ -393,7 +410,7 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
 
 #pragma unroll
   for (int s = 0; s < S; ++s)
-    if (s < nk) issue_stage<NW, LA, LB>(smem + s * STAGE_BYTES, A_BYTES, Abase, Bbase, aoff, boff, wave, s * 64);
+    if (s < nk) issue_stage<NW, LA, LB, NA, NB>(smem + s * STAGE_BYTES, A_BYTES, ra, rb, ao, bo, la, lb, wave, s * 128);
   // stage 0 complete: the later prologue stages may stay in flight
   {
     const int pend = min(S, nk) - 1;
@@ -430,8 +447,8 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
     __builtin_amdgcn_s_barrier();
     // second K half: refill this buffer with the stage S ahead and read the
     // next stage's first half, both under this half's MFMAs
-    issue_stage<NW, LA, LB>(smem + buf * STAGE_BYTES, A_BYTES, Abase, Bbase, aoff, boff, wave,
-                            min(kt + S, nk - 1) * 64);
+    issue_stage<NW, LA, LB, NA, NB>(smem + buf * STAGE_BYTES, A_BYTES, ra, rb, ao, bo, la, lb, wave,
+                                    min(kt + S, nk - 1) * 128);
     const uint8_t* nx = smem + ((kt + 1) % S) * STAGE_BYTES;
     read_frags<TM, TN>(fa0, fb0, nx + a_lane, nx + b_lane, broff);
     mfma_block<TM, TN>(acc, fa1, fb1);
@@ -678,11 +695,11 @@ struct TileCfg {
 // of at most 80 KB run two workgroups per CU. The costs were fitted to
 // MI355X timings of the layer's four GEMMs over M = 384..2374.
 constexpr TileCfg kTiles[] = {
-    {8, 4, 2, 2, 3, 0.983f, 3.8f},  {4, 8, 2, 2, 3, 0.990f, 1.9f},  {4, 4, 2, 2, 2, 0.902f, 4.7f},
-    {6, 4, 2, 2, 2, 1.018f, 15.3f}, {3, 8, 2, 2, 3, 0.833f, 1.8f},  {9, 4, 2, 2, 3, 1.087f, 1.3f},
-    {2, 8, 2, 2, 3, 0.736f, 0.0f},  {8, 4, 2, 4, 2, 1.287f, 13.1f}, {6, 4, 2, 4, 2, 1.289f, 0.0f},
-    {4, 4, 2, 4, 3, 0.855f, 5.2f},  {4, 8, 4, 2, 2, 1.282f, 13.5f}, {3, 8, 4, 2, 2, 1.274f, 1.6f},
-    {2, 8, 4, 2, 3, 0.853f, 6.4f},
+    {8, 4, 2, 2, 3, 0.991f, 0.0f}, {4, 8, 2, 2, 3, 1.052f, 0.0f}, {4, 4, 2, 2, 2, 0.989f, 0.0f},
+    {6, 4, 2, 2, 2, 1.162f, 6.2f}, {3, 8, 2, 2, 3, 0.951f, 0.0f}, {9, 4, 2, 2, 3, 1.101f, 0.0f},
+    {2, 8, 2, 2, 3, 0.829f, 0.0f}, {8, 4, 2, 4, 2, 1.589f, 0.0f}, {6, 4, 2, 4, 2, 1.479f, 0.0f},
+    {4, 4, 2, 4, 3, 1.009f, 0.0f}, {4, 8, 4, 2, 2, 1.585f, 0.0f}, {3, 8, 4, 2, 2, 1.479f, 0.0f},
+    {2, 8, 4, 2, 3, 1.008f, 0.0f}, {6, 6, 2, 4, 2, 1.692f, 2.0f},
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 
@@ -715,7 +732,8 @@ void launch_cfg(int idx, hipStream_t s, const GemmArgs& a, int tm, int tn, int k
     case 9: launch_tile<4, 4, 2, 4, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
     case 10: launch_tile<4, 8, 4, 2, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
     case 11: launch_tile<3, 8, 4, 2, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
-    default: launch_tile<2, 8, 4, 2, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 12: launch_tile<2, 8, 4, 2, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    default: launch_tile<6, 6, 2, 4, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
   }
 }
 }  // namespace
@@ -757,7 +775,7 @@ static GemmPlan search_plan(const GemmArgs& a, int cu_count, int force_cfg, int 
       const int nwg = tm * tn * ks;
       const int rounds = (nwg + slots - 1) / slots;
       double cost = rounds * (kst * c.stage_us + c.fixed_us);
-      if (ks > 1) cost += (double)a.M * W * 4.0 * (2 * ks + 1) / 6e6 + 0.7;
+      if (ks > 1) cost += (double)a.M * W * 4.0 * (2 * ks + 1) / 3.76e6 + 1.1;
       if (cost < best_cost * 0.999) {
         best_cost = cost;
         best = GemmPlan{i, tm, tn, ks, kst * 64};
@@ -768,7 +786,7 @@ static GemmPlan search_plan(const GemmArgs& a, int cu_count, int force_cfg, int 
 }
 
 GemmPlan plan_gemm(const GemmArgs& a, int cu_count, int force_cfg, int force_ksplit) {
-  if (a.K % 64 != 0) return GemmPlan{-1, 0, 0, 1, 0};
+  if (a.K % 64 != 0 || a.N % 8 != 0) return GemmPlan{-1, 0, 0, 1, 0};
   if (force_cfg >= kNumTiles) force_cfg = -1;
   // a forced shape or split that cannot run this GEMM is relaxed: first the
   // split, then the shape

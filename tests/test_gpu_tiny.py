@@ -244,7 +244,7 @@ def test_bf16_output_matches_fp32_output(hb):
     assert torch.equal(y16, ref)
 
 
-@pytest.mark.parametrize("tile", list(range(13)))
+@pytest.mark.parametrize("tile", list(range(14)))
 @pytest.mark.parametrize("ksplit", [1, 2, 3])
 def test_every_gemm_tile_shape(hb, monkeypatch, tile, ksplit):
     """Each LDS-pipelined GEMM tile shape, whole K or split (the split-K
