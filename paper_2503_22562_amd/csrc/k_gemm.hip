@@ -541,7 +541,7 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
 
 // Sum of the split-K partials in split order, then the GEMM's epilogue: for
 // the QKV GEMM the RoPE rotation of q and k and the pool scatter of k and v
-// (one work item = 4 columns of a row, with their rotation partners), for
+// (a work item is 4 columns of a row and their rotation partners), for
 // gate/up the SwiGLU product, else the residual add and the store.
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int ksplit, const float* __restrict__ partial) {
@@ -558,18 +558,19 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int kspl
   };
   const int64_t step = (int64_t)gridDim.x * 256;
   if (EPI == GEMM_QKV_ROPE) {
+    // grid (work items of a row / 256, rows): a work item is (head, 4 columns)
+    const int m = blockIdx.y;
     const int hd = a.hd, half = hd / 2, qk_heads = a.nq + a.nkv;
-    const int qk_units = qk_heads * (half / 4), per_row = qk_units + a.nkv * (hd / 4);
-    const int64_t total = (int64_t)a.M * per_row;
-    for (int64_t v = blockIdx.x * 256ll + threadIdx.x; v < total; v += step) {
-      const int m = (int)(v / per_row);
-      int r = (int)(v - (int64_t)m * per_row);
-      const int slotm = a.tok_slot[m];
-      const int blk = slotm >> 4, slot = slotm & 15;
+    const int qs = half / 4, vs = hd / 4;  // work items per q/k head, per v head (powers of two)
+    const int qs_log = __builtin_ctz(qs), vs_log = __builtin_ctz(vs);
+    const int qk_units = qk_heads * qs, units = qk_units + a.nkv * vs;
+    const int slotm = a.tok_slot[m];
+    const int blk = slotm >> 4, slot = slotm & 15;
+    const float* csr = a.rope_cs + (size_t)m * hd;
+    for (int r = blockIdx.x * 256 + threadIdx.x; r < units; r += gridDim.x * 256) {
       if (r < qk_units) {
-        const int h = r / (half / 4), j = (r - h * (half / 4)) * 4;
+        const int h = r >> qs_log, j = (r & (qs - 1)) * 4;
         const f32x4 lo = sum4(m, h * hd + j), hi = sum4(m, h * hd + half + j);
-        const float* csr = a.rope_cs + (size_t)m * hd;
         const u32x4 c4 = ld16(csr + j), s4 = ld16(csr + half + j);
         float rl[4], rh[4];
         for (int e = 0; e < 4; ++e) {
@@ -582,8 +583,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int kspl
         st8(dst + j, u32x2{pack_bf16x2(rl[0], rl[1]), pack_bf16x2(rl[2], rl[3])});
         st8(dst + half + j, u32x2{pack_bf16x2(rh[0], rh[1]), pack_bf16x2(rh[2], rh[3])});
       } else {
-        r -= qk_units;
-        const int g = r / (hd / 4), d = (r - g * (hd / 4)) * 4;
+        const int rv = r - qk_units;
+        const int g = rv >> vs_log, d = (rv & (vs - 1)) * 4;
         const f32x4 c = sum4(m, (qk_heads + g) * hd + d);
         uint16_t* vp = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * hd + ((slot >> 3) * hd + d) * 8 + (slot & 7);
         for (int e = 0; e < 4; ++e) vp[8 * e] = (uint16_t)f32_to_bf16(c[e]);
@@ -817,12 +818,12 @@ bool launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& p, float* par
     return true;
   }
   if (p.ksplit > 1) {
-    const int64_t items = a.epi == GEMM_QKV_ROPE
-                              ? (int64_t)a.M * ((a.nq + a.nkv) * (a.hd / 8) + a.nkv * (a.hd / 4))
-                              : (int64_t)a.M * a.N / 4;
-    const int grid = (int)std::min<int64_t>((items + 255) / 256, 8192);
+    const int grid = (int)std::min<int64_t>(((int64_t)a.M * a.N / 4 + 255) / 256, 8192);
+    const int row_units = (a.nq + a.nkv) * (a.hd / 8) + a.nkv * (a.hd / 4);
     switch (a.epi) {
-      case GEMM_QKV_ROPE: splitk_reduce_kernel<GEMM_QKV_ROPE><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
+      case GEMM_QKV_ROPE:
+        splitk_reduce_kernel<GEMM_QKV_ROPE><<<dim3((row_units + 255) / 256, a.M), 256, 0, s>>>(a, p.ksplit, partial);
+        break;
       case GEMM_SWIGLU: splitk_reduce_kernel<GEMM_SWIGLU><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
       case GEMM_RESIDUAL: splitk_reduce_kernel<GEMM_RESIDUAL><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
       default: splitk_reduce_kernel<GEMM_STORE_BF16><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
