@@ -27,11 +27,17 @@ constexpr int kStages = 4;
 constexpr double kPeakHbm = 8.0e12;      // MI355X HBM3E, bytes/s
 constexpr double kPeakBf16 = 2.5e15;     // MI355X dense bf16 MFMA, flop/s
 
+// One slot of the metadata ring: pinned host staging and its device copy.
+// The upload runs on the layer's copy stream, so it overlaps the previous
+// iteration's kernels; the layer's stream waits for it (copied), and the
+// next upload into the slot waits for the kernels that read it (consumed).
 struct Stage {
   int32_t* host = nullptr;  // pinned
   size_t cap = 0;           // int32 elements
-  hipEvent_t done = nullptr;
-  bool pending = false;
+  int32_t* dev = nullptr;
+  size_t dev_cap = 0;
+  hipEvent_t copied = nullptr, consumed = nullptr;
+  bool pending = false;     // copied / consumed recorded, not yet waited on by the host
 };
 
 struct TimedLaunch {
@@ -57,8 +63,7 @@ struct hb_layer {
   double* inv_freq = nullptr;
   float *part_o = nullptr, *part_ml = nullptr;
   int part_cap = 0;
-  int32_t* meta = nullptr;
-  size_t meta_cap = 0;
+  hipStream_t copy_stream = nullptr;  // metadata uploads
   float* splitk = nullptr;  // split-K partial sums
   size_t splitk_cap = 0;    // floats
   Stage stage[kStages];
@@ -76,17 +81,6 @@ struct hb_layer {
 
 namespace {
 
-hb_status ensure_meta(hb_layer* L, size_t n) {
-  if (n <= L->meta_cap) return HB_OK;
-  size_t cap = std::max(n, L->meta_cap * 2);
-  HB_HIP(hipStreamSynchronize(L->stream));
-  if (L->meta) HB_HIP(hipFree(L->meta));
-  L->meta = nullptr;
-  L->meta_cap = 0;
-  if (hipMalloc(&L->meta, cap * sizeof(int32_t)) != hipSuccess) return fail(HB_ERR_OOM, "metadata buffer of %zu B", cap * 4);
-  L->meta_cap = cap;
-  return HB_OK;
-}
 
 hb_status ensure_splitk(hb_layer* L, size_t floats) {
   if (floats <= L->splitk_cap) return HB_OK;
@@ -116,12 +110,15 @@ hb_status ensure_parts(hb_layer* L, int n) {
   return HB_OK;
 }
 
-// Copy `n` int32 from host to L->meta through the pinned staging ring.
-hb_status stage_upload(hb_layer* L, const int32_t* src, size_t n, int32_t* dst) {
-  Stage& s = L->stage[L->stage_next];
+// Upload `n` int32 through the next slot of the staging ring; *dev receives
+// the slot's device copy, valid for the work enqueued on the layer's stream
+// until stage_consumed(L, slot) is called after that work.
+hb_status stage_upload(hb_layer* L, const int32_t* src, size_t n, const int32_t** dev, int* slot) {
+  const int k = L->stage_next;
+  Stage& s = L->stage[k];
   L->stage_next = (L->stage_next + 1) % kStages;
   if (s.pending) {
-    HB_HIP(hipEventSynchronize(s.done));
+    HB_HIP(hipEventSynchronize(s.copied));  // the host buffer is free again
     s.pending = false;
   }
   if (n > s.cap) {
@@ -133,10 +130,29 @@ hb_status stage_upload(hb_layer* L, const int32_t* src, size_t n, int32_t* dst) 
       return fail(HB_ERR_OOM, "pinned staging of %zu B", cap * 4);
     s.cap = cap;
   }
+  if (n > s.dev_cap) {
+    HB_HIP(hipEventSynchronize(s.consumed));  // no kernel reads the old copy any more
+    if (s.dev) HB_HIP(hipFree(s.dev));
+    s.dev = nullptr;
+    s.dev_cap = 0;
+    size_t cap = std::max<size_t>(n, 1 << 16);
+    if (hipMalloc(&s.dev, cap * sizeof(int32_t)) != hipSuccess)
+      return fail(HB_ERR_OOM, "metadata buffer of %zu B", cap * 4);
+    s.dev_cap = cap;
+  }
   std::memcpy(s.host, src, n * sizeof(int32_t));
-  HB_HIP(hipMemcpyAsync(dst, s.host, n * sizeof(int32_t), hipMemcpyHostToDevice, L->stream));
-  HB_HIP(hipEventRecord(s.done, L->stream));
+  HB_HIP(hipStreamWaitEvent(L->copy_stream, s.consumed, 0));
+  HB_HIP(hipMemcpyAsync(s.dev, s.host, n * sizeof(int32_t), hipMemcpyHostToDevice, L->copy_stream));
+  HB_HIP(hipEventRecord(s.copied, L->copy_stream));
+  HB_HIP(hipStreamWaitEvent(L->stream, s.copied, 0));
   s.pending = true;
+  *dev = s.dev;
+  *slot = k;
+  return HB_OK;
+}
+
+hb_status stage_consumed(hb_layer* L, int slot) {
+  HB_HIP(hipEventRecord(L->stage[slot].consumed, L->stream));
   return HB_OK;
 }
 
@@ -192,12 +208,16 @@ void free_layer(hb_layer* L) {
   if (!L) return;
   (void)hipStreamSynchronize(L->stream);
   for (void* p : {(void*)L->xn, (void*)L->rope_cs, (void*)L->tok_slot, (void*)L->q_rot, (void*)L->attn, (void*)L->mlp, (void*)L->h2,
-                  (void*)L->inv_freq, (void*)L->part_o, (void*)L->part_ml, (void*)L->meta, (void*)L->splitk})
+                  (void*)L->inv_freq, (void*)L->part_o, (void*)L->part_ml, (void*)L->splitk})
     if (p) (void)hipFree(p);
+  if (L->copy_stream) (void)hipStreamSynchronize(L->copy_stream);
   for (Stage& s : L->stage) {
     if (s.host) (void)hipHostFree(s.host);
-    if (s.done) (void)hipEventDestroy(s.done);
+    if (s.dev) (void)hipFree(s.dev);
+    if (s.copied) (void)hipEventDestroy(s.copied);
+    if (s.consumed) (void)hipEventDestroy(s.consumed);
   }
+  if (L->copy_stream) (void)hipStreamDestroy(L->copy_stream);
   for (const TimedLaunch& t : L->timed) {
     (void)hipEventDestroy(t.start);
     (void)hipEventDestroy(t.stop);
@@ -256,13 +276,19 @@ hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
                                 std::make_pair(pd, gd)})
     if (pl.ksplit > 1) sk = std::max(sk, (size_t)pl.ksplit * ga.M * partial_width(ga));
 
-  hb_status st = ensure_meta(L, p.meta.size());
-  if (st == HB_OK) st = ensure_parts(L, p.n_slots);
+  hb_status st = ensure_parts(L, p.n_slots);
   if (st == HB_OK) st = ensure_splitk(L, sk);
   if (st != HB_OK) return st;
-  st = stage_upload(L, p.meta.data(), p.meta.size(), L->meta);
+  const int32_t* meta = nullptr;
+  int slot = 0;
+  st = stage_upload(L, p.meta.data(), p.meta.size(), &meta, &slot);
   if (st != HB_OK) return st;
-  const int32_t* meta = L->meta;
+  // the slot may be refilled once everything enqueued below has run
+  struct Consumed {
+    hb_layer* L;
+    int slot;
+    ~Consumed() { (void)stage_consumed(L, slot); }
+  } consumed{L, slot};
 
   RopePrep rp{};
   rp.tok_pos = meta + p.off_tok_pos; rp.tok_req = meta + p.off_tok_req;
@@ -378,11 +404,13 @@ hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w,
   for (int j = 0; j < d.hd / 2; ++j) inv[j] = std::pow((double)d.theta, -2.0 * j / d.hd);
   if (hipMemcpy(L->inv_freq, inv.data(), inv.size() * sizeof(double), hipMemcpyHostToDevice) != hipSuccess)
     return bail(fail(HB_ERR_HIP, "upload of RoPE frequencies failed"));
+  if (hipStreamCreateWithFlags(&L->copy_stream, hipStreamNonBlocking) != hipSuccess)
+    return bail(fail(HB_ERR_HIP, "hipStreamCreate failed"));
   for (Stage& s : L->stage)
-    if (hipEventCreateWithFlags(&s.done, hipEventDisableTiming) != hipSuccess)
+    if (hipEventCreateWithFlags(&s.copied, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&s.consumed, hipEventDisableTiming) != hipSuccess)
       return bail(fail(HB_ERR_HIP, "hipEventCreate failed"));
-  st = ensure_meta(L, (size_t)1 << 18);
-  if (st == HB_OK) st = ensure_parts(L, 1 << 16);
+  st = ensure_parts(L, 1 << 16);
   if (st != HB_OK) return bail(st);
   *out = L;
   return HB_OK;
@@ -404,13 +432,15 @@ hb_status hb_append_kv(hb_layer* L, const int32_t* block_table, int32_t n_blocks
     if (block_table[i] < 0 || block_table[i] >= L->pool.num_blocks)
       return fail(HB_ERR_RANGE, "block_table[%lld] = %d outside [0, %d)", (long long)i, block_table[i],
                   L->pool.num_blocks);
-  hb_status st = ensure_meta(L, (size_t)nb);
-  if (st != HB_OK) return st;
-  st = stage_upload(L, block_table, (size_t)nb, L->meta);
+  const int32_t* bt = nullptr;
+  int slot = 0;
+  hb_status st = stage_upload(L, block_table, (size_t)nb, &bt, &slot);
   if (st != HB_OK) return st;
   launch_append_kv(L->stream, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), n_tokens,
-                   context_len, L->meta, L->d.nkv, L->d.hd, static_cast<uint16_t*>(L->pool.k_pool),
+                   context_len, bt, L->d.nkv, L->d.hd, static_cast<uint16_t*>(L->pool.k_pool),
                    static_cast<uint16_t*>(L->pool.v_pool));
+  st = stage_consumed(L, slot);
+  if (st != HB_OK) return st;
   return check_hip("append_kv launch");
 }
 
