@@ -322,26 +322,28 @@ struct TileGeom {
 template <int HD>
 __device__ __forceinline__ void tile_issue(uint8_t* stage, const AttnArgs& a, int id, int g, int wave, int lane) {
   using TG = TileGeom<HD>;
+  typedef __attribute__((address_space(3))) void* lds_ptr;
   const int b = wave;
-  const size_t blk_stride = (size_t)a.nkv * 16 * HD;
-  const size_t off = (size_t)id * blk_stride + (size_t)g * 16 * HD;
+  // a buffer resource over this wave's 4-KB block (K or V of pool block b & 1):
+  // the loads then carry only a lane offset and a scalar offset
+  const uint16_t* blk = (b < 2 ? a.k_pool : a.v_pool) + ((size_t)id * a.nkv + g) * 16 * HD;
+  const __amdgpu_buffer_rsrc_t r =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(blk), (short)0, TG::BLK, 0x00020000);
+  uint8_t* dst = stage + b * TG::BLK;  // K of both blocks, then V of both
   if (b < 2) {
-    uint8_t* dst = stage + b * TG::BLK;
-    const uint16_t* K = a.k_pool + off;
     const int kk_lane = lane / TG::CHUNKS, pc = lane % TG::CHUNKS;
 #pragma unroll
     for (int i = 0; i < TG::LOADS; ++i) {
       const int kk = i * TG::KEYS_PER_LOAD + kk_lane;
-      const uint16_t* src = K + kk * HD + 8 * (pc ^ TG::kswz(b, kk));
-      __builtin_amdgcn_global_load_lds(src, dst + i * 1024, 16, 0, 0);
+      const uint32_t voff = 2u * (uint32_t)(kk_lane * HD + 8 * (pc ^ TG::kswz(b, kk)));
+      uint8_t* d = dst + i * 1024;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)d, 16, voff, (uint32_t)(i * 1024), 0, 0);
     }
   } else {
-    uint8_t* dst = stage + 2 * TG::BLK + (b - 2) * TG::BLK;
-    const uint8_t* V = reinterpret_cast<const uint8_t*>(a.v_pool + off);
 #pragma unroll
     for (int i = 0; i < TG::LOADS; ++i) {
       uint8_t* d = dst + i * 1024;
-      __builtin_amdgcn_global_load_lds(V + i * 1024 + lane * 16, d, 16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)d, 16, (uint32_t)(lane * 16), (uint32_t)(i * 1024), 0, 0);
     }
   }
 }
