@@ -152,6 +152,27 @@ def copy_calibration(nbytes=1 << 30, reps=3):
     return 0
 
 
+def regime(hb, dl, batch, shape, x_dev, y_dev, steps):
+    """Per-kernel timing of one sweep cell: every launch bracketed by HIP
+    events, the cell run `steps` times after two warm-up iterations."""
+    reqs = [(q.chunk_len, q.context_len, q.block_table) for q in batch.requests]
+    for _ in range(2):
+        dl.run(reqs, x_dev, hb.HB_OUT_F32, y_dev)
+    hb.hb_set_kernel_timing(dl.layer, True)
+    hb.hb_kernel_times(dl.layer, reset=True)
+    for _ in range(steps):
+        dl.run(reqs, x_dev, hb.HB_OUT_F32, y_dev)
+    times = hb.hb_kernel_times(dl.layer, reset=True)
+    hb.hb_set_kernel_timing(dl.layer, False)
+    work = kernel_work(shape, [(c, xx) for c, xx, _ in reqs])
+    out = {}
+    for name, (tot, n) in times.items():
+        if n:
+            fl, by = work.get(name, (0.0, 0.0))
+            out[name] = (tot / n * 1e-3, fl, by)
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -160,6 +181,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--profile-iters", type=int, default=15)
+    ap.add_argument("--regime-steps", type=int, default=10)
+    ap.add_argument("--no-regimes", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration) and exit")
     a = ap.parse_args()
@@ -267,6 +290,36 @@ def main() -> int:
     flops, bytes_ = layer_work(shape, [(c, xx) for c, xx, _ in reqs])
     step_s = ms_per_step * 1e-3
 
+    # the two regimes the layer's targets name: attention's HBM rate on a
+    # decode-heavy batch, the GEMMs' MFMA rate on a chunk-heavy one
+    from hb_workloads import sweep_batch
+    regimes = None if a.no_regimes else {}
+    if regimes is not None:
+        dec = sweep_batch(128, 256)
+        xd = to_device_bf16(dec.x_in())
+        yd = torch.empty((dec.n_tokens, shape.hidden), dtype=torch.float32, device="cuda")
+        kt = regime(hb, dl, dec, shape, xd, yd, a.regime_steps)
+        at_s, _, at_b = kt["attention"]
+        regimes["decode_heavy"] = {
+            "cell": "chunk 128 + 256 decodes, contexts log-uniform 256..8192",
+            "kernel": "attention", "avg_ms": round(at_s * 1e3, 5), "gbps": round(at_b / at_s / 1e9, 1),
+            "hbm_frac": round(at_b / at_s / PEAK_HBM, 4),
+            "layer_ms": round(sum(t for t, _, _ in kt.values()) * 1e3, 4)}
+        chk = sweep_batch(2048, 0)
+        xc = to_device_bf16(chk.x_in())
+        yc = torch.empty((chk.n_tokens, shape.hidden), dtype=torch.float32, device="cuda")
+        kt = regime(hb, dl, chk, shape, xc, yc, a.regime_steps)
+        gem = {k: v for k, v in kt.items() if k.startswith("gemm_")}
+        g_s = sum(t for t, _, _ in gem.values())
+        g_f = sum(f for _, f, _ in gem.values())
+        regimes["chunk_heavy"] = {
+            "cell": "chunk 2048 + 0 decodes", "kernels": "the four GEMMs (split-K reduces included)",
+            "avg_ms": round(g_s * 1e3, 5), "tflops": round(g_f / g_s / 1e12, 1),
+            "mfma_frac": round(g_f / g_s / PEAK_BF16, 4),
+            "per_gemm_tflops": {k: round(f / t / 1e12, 1) for k, (t, f, _) in sorted(gem.items())},
+            "layer_ms": round(sum(t for t, _, _ in kt.values()) * 1e3, 4)}
+        del xd, yd, xc, yc
+
     profile = None
     if not a.no_profile:
         log("bench: latency profile (chunk x decode grid)")
@@ -320,6 +373,8 @@ def main() -> int:
         "kernels": kernels,
         "kernels_note": "per-kernel averages from a separate pass with every launch bracketed by events",
         "cpu_baseline": cpu,
+        "regimes": regimes,
+        "regimes_note": "per-kernel averages with every launch bracketed by events; algorithmic work as for roofline",
         "latency_profile": profile,
     }
     print(json.dumps(out), flush=True)

@@ -543,51 +543,63 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
 // the QKV GEMM the RoPE rotation of q and k and the pool scatter of k and v
 // (a work item is 4 columns of a row and their rotation partners), for
 // gate/up the SwiGLU product, else the residual add and the store.
-template <int EPI>
-__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int ksplit, const float* __restrict__ partial) {
+// Largest K split the planner chooses; the reduce kernels are instantiated
+// per split count so that all of a work item's partial loads are in flight
+// together.
+constexpr int kMaxKSplit = 8;
+
+// Four consecutive fp32 partials summed over the KS splits, in split order.
+template <int KS>
+__device__ __forceinline__ f32x4 sum_splits(const float* p, size_t stride) {
+  u32x4 v[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) v[s] = ld16(p + s * stride);
+  f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < KS; ++s)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[j] += __uint_as_float(v[s][j]);
+  return c;
+}
+
+template <int EPI, int KS>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, const float* __restrict__ partial) {
   const int W = (EPI == GEMM_SWIGLU) ? 2 * a.N : a.N;
   const size_t split_stride = (size_t)a.M * W;
-  auto sum4 = [&](int m, int n) {
-    f32x4 c = {0.f, 0.f, 0.f, 0.f};
-    const float* p = partial + (size_t)m * W + n;
-    for (int s = 0; s < ksplit; ++s) {
-      const u32x4 v = ld16(p + s * split_stride);
-      for (int j = 0; j < 4; ++j) c[j] += __uint_as_float(v[j]);
-    }
-    return c;
-  };
+  auto sum4 = [&](int m, int n) { return sum_splits<KS>(partial + (size_t)m * W + n, split_stride); };
   const int64_t step = (int64_t)gridDim.x * 256;
   if (EPI == GEMM_QKV_ROPE) {
-    // grid (work items of a row / 256, rows): a work item is (head, 4 columns)
-    const int m = blockIdx.y;
+    // grid (work items of a row / 256, row groups): a work item is (head, 4 columns)
     const int hd = a.hd, half = hd / 2, qk_heads = a.nq + a.nkv;
     const int qs = half / 4, vs = hd / 4;  // work items per q/k head, per v head (powers of two)
     const int qs_log = __builtin_ctz(qs), vs_log = __builtin_ctz(vs);
     const int qk_units = qk_heads * qs, units = qk_units + a.nkv * vs;
-    const int slotm = a.tok_slot[m];
-    const int blk = slotm >> 4, slot = slotm & 15;
-    const float* csr = a.rope_cs + (size_t)m * hd;
-    for (int r = blockIdx.x * 256 + threadIdx.x; r < units; r += gridDim.x * 256) {
-      if (r < qk_units) {
-        const int h = r >> qs_log, j = (r & (qs - 1)) * 4;
-        const f32x4 lo = sum4(m, h * hd + j), hi = sum4(m, h * hd + half + j);
-        const u32x4 c4 = ld16(csr + j), s4 = ld16(csr + half + j);
-        float rl[4], rh[4];
-        for (int e = 0; e < 4; ++e) {
-          const float c = __uint_as_float(c4[e]), sn = __uint_as_float(s4[e]);
-          rl[e] = lo[e] * c - hi[e] * sn;
-          rh[e] = hi[e] * c + lo[e] * sn;
+    for (int m = blockIdx.y; m < a.M; m += gridDim.y) {
+      const int slotm = a.tok_slot[m];
+      const int blk = slotm >> 4, slot = slotm & 15;
+      const float* csr = a.rope_cs + (size_t)m * hd;
+      for (int r = blockIdx.x * 256 + threadIdx.x; r < units; r += gridDim.x * 256) {
+        if (r < qk_units) {
+          const int h = r >> qs_log, j = (r & (qs - 1)) * 4;
+          const f32x4 lo = sum4(m, h * hd + j), hi = sum4(m, h * hd + half + j);
+          const u32x4 c4 = ld16(csr + j), s4 = ld16(csr + half + j);
+          float rl[4], rh[4];
+          for (int e = 0; e < 4; ++e) {
+            const float c = __uint_as_float(c4[e]), sn = __uint_as_float(s4[e]);
+            rl[e] = lo[e] * c - hi[e] * sn;
+            rh[e] = hi[e] * c + lo[e] * sn;
+          }
+          uint16_t* dst = h < a.nq ? reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + h * hd
+                                   : a.k_pool + (((size_t)blk * a.nkv + (h - a.nq)) * 16 + slot) * hd;
+          st8(dst + j, u32x2{pack_bf16x2(rl[0], rl[1]), pack_bf16x2(rl[2], rl[3])});
+          st8(dst + half + j, u32x2{pack_bf16x2(rh[0], rh[1]), pack_bf16x2(rh[2], rh[3])});
+        } else {
+          const int rv = r - qk_units;
+          const int g = rv >> vs_log, d = (rv & (vs - 1)) * 4;
+          const f32x4 c = sum4(m, (qk_heads + g) * hd + d);
+          uint16_t* vp = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * hd + ((slot >> 3) * hd + d) * 8 + (slot & 7);
+          for (int e = 0; e < 4; ++e) vp[8 * e] = (uint16_t)f32_to_bf16(c[e]);
         }
-        uint16_t* dst = h < a.nq ? reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + h * hd
-                                 : a.k_pool + (((size_t)blk * a.nkv + (h - a.nq)) * 16 + slot) * hd;
-        st8(dst + j, u32x2{pack_bf16x2(rl[0], rl[1]), pack_bf16x2(rl[2], rl[3])});
-        st8(dst + half + j, u32x2{pack_bf16x2(rh[0], rh[1]), pack_bf16x2(rh[2], rh[3])});
-      } else {
-        const int rv = r - qk_units;
-        const int g = rv >> vs_log, d = (rv & (vs - 1)) * 4;
-        const f32x4 c = sum4(m, (qk_heads + g) * hd + d);
-        uint16_t* vp = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * hd + ((slot >> 3) * hd + d) * 8 + (slot & 7);
-        for (int e = 0; e < 4; ++e) vp[8 * e] = (uint16_t)f32_to_bf16(c[e]);
       }
     }
     return;
@@ -628,9 +640,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int kspl
 // follows it: one workgroup per row sums the partials in split order, adds the
 // residual, stores the row (fp32) and normalises it into norm_out (bf16), with
 // the same element-to-thread mapping and reduction order as the RMSNorm kernel.
-template <int MAXV>
-__global__ __launch_bounds__(256) void splitk_reduce_rmsnorm_kernel(GemmArgs a, int ksplit,
-                                                                    const float* __restrict__ partial) {
+template <int MAXV, int KS>
+__global__ __launch_bounds__(256) void splitk_reduce_rmsnorm_kernel(GemmArgs a, const float* __restrict__ partial) {
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x, N = a.N;
   const int nvec = N >> 3;
@@ -642,11 +653,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_rmsnorm_kernel(GemmArgs a, 
     const int vi = tid + 256 * i;
     if (vi < nvec) {
       const float* p = partial + (size_t)row * N + 8 * vi;
-      float c[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      for (int s = 0; s < ksplit; ++s) {
-        const u32x4 x0 = ld16(p + s * split_stride), x1 = ld16(p + s * split_stride + 4);
-        for (int j = 0; j < 4; ++j) { c[j] += __uint_as_float(x0[j]); c[4 + j] += __uint_as_float(x1[j]); }
-      }
+      const f32x4 c0 = sum_splits<KS>(p, split_stride), c1 = sum_splits<KS>(p + 4, split_stride);
+      float c[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
       if (a.r_f32) {
         const float* rr = reinterpret_cast<const float*>(a.R) + (size_t)row * a.ldr + 8 * vi;
         const u32x4 r0 = ld16(rr), r1 = ld16(rr + 4);
@@ -689,18 +697,25 @@ using namespace gemm_detail;
 
 struct TileCfg {
   int tm, tn, wr, wc, stages;  // per-wave MFMA blocks, wave grid, LDS stages
-  float stage_us, fixed_us;    // measured cost of one 64-wide K stage per round, and per round
+  // measured cost (us) of one 64-wide K stage: in a launch's first round with
+  // one workgroup per CU, in a first round with two per CU (4-wave tiles with
+  // small LDS rings only), in each later round (the weights then come from
+  // the caches, not HBM); and a fixed cost per round
+  float first_alone_us, first_pair_us, next_us, fixed_us;
 };
 // Accumulators and both fragment sets stay within the 256 VGPRs of a wave.
 // 8-wave workgroups put two waves on each SIMD; 4-wave ones with LDS rings
 // of at most 80 KB run two workgroups per CU. The costs were fitted to
-// MI355X timings of the layer's four GEMMs over M = 384..2374.
+// MI355X timings of the layer's four GEMMs at M = 384, 576, 1056, 2048 and
+// 2374 (14 shapes x splits 1, 2, 3, 4, 6, 8).
 constexpr TileCfg kTiles[] = {
-    {8, 4, 2, 2, 3, 0.991f, 0.0f}, {4, 8, 2, 2, 3, 1.052f, 0.0f}, {4, 4, 2, 2, 2, 0.989f, 0.0f},
-    {6, 4, 2, 2, 2, 1.162f, 6.2f}, {3, 8, 2, 2, 3, 0.951f, 0.0f}, {9, 4, 2, 2, 3, 1.101f, 0.0f},
-    {2, 8, 2, 2, 3, 0.829f, 0.0f}, {8, 4, 2, 4, 2, 1.589f, 0.0f}, {6, 4, 2, 4, 2, 1.479f, 0.0f},
-    {4, 4, 2, 4, 3, 1.009f, 0.0f}, {4, 8, 4, 2, 2, 1.585f, 0.0f}, {3, 8, 4, 2, 2, 1.479f, 0.0f},
-    {2, 8, 4, 2, 3, 1.008f, 0.0f}, {6, 6, 2, 4, 2, 1.692f, 2.0f},
+    {8, 4, 2, 2, 3, 0.978f, 0.978f, 0.920f, 0.00f},  {4, 8, 2, 2, 3, 1.046f, 1.046f, 0.850f, 4.61f},
+    {4, 4, 2, 2, 2, 0.849f, 1.040f, 0.798f, 9.68f},  {6, 4, 2, 2, 2, 1.012f, 1.458f, 1.260f, 1.14f},
+    {3, 8, 2, 2, 3, 0.961f, 0.961f, 0.779f, 0.00f},  {9, 4, 2, 2, 3, 1.073f, 1.073f, 1.039f, 0.00f},
+    {2, 8, 2, 2, 3, 0.911f, 0.911f, 0.690f, 0.00f},  {8, 4, 2, 4, 2, 1.525f, 1.525f, 1.353f, 8.74f},
+    {6, 4, 2, 4, 2, 1.411f, 1.411f, 1.188f, 7.69f},  {4, 4, 2, 4, 3, 0.999f, 0.999f, 0.863f, 2.13f},
+    {4, 8, 4, 2, 2, 1.512f, 1.512f, 1.305f, 10.75f}, {3, 8, 4, 2, 2, 1.427f, 1.427f, 1.235f, 5.37f},
+    {2, 8, 4, 2, 3, 1.000f, 1.000f, 0.857f, 4.33f},  {6, 6, 2, 4, 2, 1.636f, 1.636f, 1.499f, 12.96f},
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 
@@ -737,6 +752,52 @@ void launch_cfg(int idx, hipStream_t s, const GemmArgs& a, int tm, int tn, int k
     default: launch_tile<6, 6, 2, 4, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
   }
 }
+
+// The reduce grids fit one wave of workgroups over the chip (about four per
+// CU), each thread looping over an equal share of the work items: short
+// workgroups in a second, mostly empty round cost more than the loop.
+constexpr int kReduceWgs = 1024;
+
+template <int EPI, int KS>
+void launch_reduce_ks(hipStream_t s, const GemmArgs& a, const float* partial) {
+  if (EPI == GEMM_QKV_ROPE) {
+    const int row_units = (a.nq + a.nkv) * (a.hd / 8) + a.nkv * (a.hd / 4);
+    const int gx = (row_units + 255) / 256;
+    const int rows_per_wg = (a.M * gx + kReduceWgs - 1) / kReduceWgs;
+    splitk_reduce_kernel<EPI, KS><<<dim3(gx, (a.M + rows_per_wg - 1) / rows_per_wg), 256, 0, s>>>(a, partial);
+  } else {
+    const int64_t wgs = ((int64_t)a.M * a.N / 4 + 255) / 256;
+    const int64_t per = (wgs + kReduceWgs - 1) / kReduceWgs;
+    splitk_reduce_kernel<EPI, KS><<<(int)((wgs + per - 1) / per), 256, 0, s>>>(a, partial);
+  }
+}
+
+template <int EPI>
+void launch_reduce(hipStream_t s, const GemmArgs& a, int ks, const float* partial) {
+  static_assert(kMaxKSplit == 8, "one case per split count");
+  switch (ks) {
+    case 2: launch_reduce_ks<EPI, 2>(s, a, partial); break;
+    case 3: launch_reduce_ks<EPI, 3>(s, a, partial); break;
+    case 4: launch_reduce_ks<EPI, 4>(s, a, partial); break;
+    case 5: launch_reduce_ks<EPI, 5>(s, a, partial); break;
+    case 6: launch_reduce_ks<EPI, 6>(s, a, partial); break;
+    case 7: launch_reduce_ks<EPI, 7>(s, a, partial); break;
+    default: launch_reduce_ks<EPI, 8>(s, a, partial); break;
+  }
+}
+
+template <int MAXV>
+void launch_reduce_rmsnorm(hipStream_t s, const GemmArgs& a, int ks, const float* partial) {
+  switch (ks) {
+    case 2: splitk_reduce_rmsnorm_kernel<MAXV, 2><<<a.M, 256, 0, s>>>(a, partial); break;
+    case 3: splitk_reduce_rmsnorm_kernel<MAXV, 3><<<a.M, 256, 0, s>>>(a, partial); break;
+    case 4: splitk_reduce_rmsnorm_kernel<MAXV, 4><<<a.M, 256, 0, s>>>(a, partial); break;
+    case 5: splitk_reduce_rmsnorm_kernel<MAXV, 5><<<a.M, 256, 0, s>>>(a, partial); break;
+    case 6: splitk_reduce_rmsnorm_kernel<MAXV, 6><<<a.M, 256, 0, s>>>(a, partial); break;
+    case 7: splitk_reduce_rmsnorm_kernel<MAXV, 7><<<a.M, 256, 0, s>>>(a, partial); break;
+    default: splitk_reduce_rmsnorm_kernel<MAXV, 8><<<a.M, 256, 0, s>>>(a, partial); break;
+  }
+}
 }  // namespace
 
 int gemm_tile_count() { return kNumTiles; }
@@ -744,9 +805,10 @@ int gemm_tile_count() { return kNumTiles; }
 int partial_width(const GemmArgs& a) { return a.epi == GEMM_SWIGLU ? 2 * a.N : a.N; }
 
 // Cost model (microseconds): workgroups run in rounds of one (two, for small
-// LDS rings) per CU, each round costing its K stages at the tile's measured
-// rate; a K split adds the fp32 partials' round trip through HBM and the
-// reduce launch.
+// LDS rings) per CU; the first round costs its K stages at the tile's
+// first-round rate (for one or two workgroups per CU), every later round at
+// the later-round rate, plus a fixed cost per round; a K split adds the fp32
+// partials' round trip (fitted at 5.1 TB/s) and the reduce launch.
 static int tiles_per_cu(const TileCfg& c) {
   const int lds = c.stages * 16 * (c.tm * c.wr + c.tn * c.wc) * 128;
   return (c.wr * c.wc == 4 && 2 * lds <= 160 * 1024) ? 2 : 1;
@@ -767,16 +829,18 @@ static GemmPlan search_plan(const GemmArgs& a, int cu_count, int force_cfg, int 
     const int ncols = (a.epi == GEMM_SWIGLU) ? bn / 2 : bn;
     const int tm = (a.M + bm - 1) / bm, tn = (a.N + ncols - 1) / ncols;
     const int slots = std::max(1, cu_count) * tiles_per_cu(c);
-    for (int ks = 1; ks <= 8; ++ks) {
+    for (int ks = 1; ks <= kMaxKSplit; ++ks) {
       if (ks > 1 && ksteps < 4 * ks) break;
       if (force_ksplit > 0 && ks != force_ksplit) continue;
       if (!fits(c, ks)) continue;
       const int kst = (ksteps + ks - 1) / ks;
       if ((ks - 1) * kst >= ksteps) continue;  // every split gets at least one stage
       const int nwg = tm * tn * ks;
+      const int cus = std::max(1, cu_count);
       const int rounds = (nwg + slots - 1) / slots;
-      double cost = rounds * (kst * c.stage_us + c.fixed_us);
-      if (ks > 1) cost += (double)a.M * W * 4.0 * (2 * ks + 1) / 3.76e6 + 1.1;
+      const float first = (slots > cus && nwg > cus) ? c.first_pair_us : c.first_alone_us;
+      double cost = kst * (first + (rounds - 1) * c.next_us) + rounds * c.fixed_us;
+      if (ks > 1) cost += (double)a.M * W * 4.0 * (2 * ks + 1) / 5.12e6 + 1.6;
       if (cost < best_cost * 0.999) {
         best_cost = cost;
         best = GemmPlan{i, tm, tn, ks, kst * 64};
@@ -812,21 +876,17 @@ bool launch_gemm(hipStream_t s, const GemmArgs& a, const GemmPlan& p, float* par
   if (p.ksplit > 1 && a.epi == GEMM_RESIDUAL && a.c_f32 && a.norm_out && a.N % 8 == 0 && a.ldc == a.N &&
       a.N <= 8 * 256 * 8) {
     const int nvec = a.N / 8;
-    if (nvec <= 256) splitk_reduce_rmsnorm_kernel<1><<<a.M, 256, 0, s>>>(a, p.ksplit, partial);
-    else if (nvec <= 1024) splitk_reduce_rmsnorm_kernel<4><<<a.M, 256, 0, s>>>(a, p.ksplit, partial);
-    else splitk_reduce_rmsnorm_kernel<8><<<a.M, 256, 0, s>>>(a, p.ksplit, partial);
+    if (nvec <= 256) launch_reduce_rmsnorm<1>(s, a, p.ksplit, partial);
+    else if (nvec <= 1024) launch_reduce_rmsnorm<4>(s, a, p.ksplit, partial);
+    else launch_reduce_rmsnorm<8>(s, a, p.ksplit, partial);
     return true;
   }
   if (p.ksplit > 1) {
-    const int grid = (int)std::min<int64_t>(((int64_t)a.M * a.N / 4 + 255) / 256, 8192);
-    const int row_units = (a.nq + a.nkv) * (a.hd / 8) + a.nkv * (a.hd / 4);
     switch (a.epi) {
-      case GEMM_QKV_ROPE:
-        splitk_reduce_kernel<GEMM_QKV_ROPE><<<dim3((row_units + 255) / 256, a.M), 256, 0, s>>>(a, p.ksplit, partial);
-        break;
-      case GEMM_SWIGLU: splitk_reduce_kernel<GEMM_SWIGLU><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
-      case GEMM_RESIDUAL: splitk_reduce_kernel<GEMM_RESIDUAL><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
-      default: splitk_reduce_kernel<GEMM_STORE_BF16><<<grid, 256, 0, s>>>(a, p.ksplit, partial); break;
+      case GEMM_QKV_ROPE: launch_reduce<GEMM_QKV_ROPE>(s, a, p.ksplit, partial); break;
+      case GEMM_SWIGLU: launch_reduce<GEMM_SWIGLU>(s, a, p.ksplit, partial); break;
+      case GEMM_RESIDUAL: launch_reduce<GEMM_RESIDUAL>(s, a, p.ksplit, partial); break;
+      default: launch_reduce<GEMM_STORE_BF16>(s, a, p.ksplit, partial); break;
     }
   }
   return false;
