@@ -569,39 +569,51 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, const fl
   auto sum4 = [&](int m, int n) { return sum_splits<KS>(partial + (size_t)m * W + n, split_stride); };
   const int64_t step = (int64_t)gridDim.x * 256;
   if (EPI == GEMM_QKV_ROPE) {
-    // grid (work items of a row / 256, row groups): a work item is (head, 4 columns)
+    // Workgroups [0, M * qk_wgs): one row each, a thread one (q or k head,
+    // 4 columns and their rotation partners). The rest: V, one wave item of
+    // (kv head, 32 dimensions, 8 consecutive rows) per wave, lane = (row
+    // lane % 8, 4 dimensions lane / 8), so the 8 lanes of a dimension write
+    // the 8 slots of one 16-byte V group together: a chunk's V lines are
+    // written whole by one wave instead of 2 bytes at a time.
     const int hd = a.hd, half = hd / 2, qk_heads = a.nq + a.nkv;
-    const int qs = half / 4, vs = hd / 4;  // work items per q/k head, per v head (powers of two)
-    const int qs_log = __builtin_ctz(qs), vs_log = __builtin_ctz(vs);
-    const int qk_units = qk_heads * qs, units = qk_units + a.nkv * vs;
-    for (int m = blockIdx.y; m < a.M; m += gridDim.y) {
-      const int slotm = a.tok_slot[m];
-      const int blk = slotm >> 4, slot = slotm & 15;
+    const int qs = half / 4;  // work items per q/k head (a power of two)
+    const int qs_log = __builtin_ctz(qs);
+    const int qk_units = qk_heads * qs, qk_wgs = (qk_units + 255) / 256;
+    const int b = blockIdx.x;
+    if (b < a.M * qk_wgs) {
+      const int m = b / qk_wgs, r = (b - m * qk_wgs) * 256 + threadIdx.x;
+      if (r >= qk_units) return;
+      const int h = r >> qs_log, j = (r & (qs - 1)) * 4;
       const float* csr = a.rope_cs + (size_t)m * hd;
-      for (int r = blockIdx.x * 256 + threadIdx.x; r < units; r += gridDim.x * 256) {
-        if (r < qk_units) {
-          const int h = r >> qs_log, j = (r & (qs - 1)) * 4;
-          const f32x4 lo = sum4(m, h * hd + j), hi = sum4(m, h * hd + half + j);
-          const u32x4 c4 = ld16(csr + j), s4 = ld16(csr + half + j);
-          float rl[4], rh[4];
-          for (int e = 0; e < 4; ++e) {
-            const float c = __uint_as_float(c4[e]), sn = __uint_as_float(s4[e]);
-            rl[e] = lo[e] * c - hi[e] * sn;
-            rh[e] = hi[e] * c + lo[e] * sn;
-          }
-          uint16_t* dst = h < a.nq ? reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + h * hd
-                                   : a.k_pool + (((size_t)blk * a.nkv + (h - a.nq)) * 16 + slot) * hd;
-          st8(dst + j, u32x2{pack_bf16x2(rl[0], rl[1]), pack_bf16x2(rl[2], rl[3])});
-          st8(dst + half + j, u32x2{pack_bf16x2(rh[0], rh[1]), pack_bf16x2(rh[2], rh[3])});
-        } else {
-          const int rv = r - qk_units;
-          const int g = rv >> vs_log, d = (rv & (vs - 1)) * 4;
-          const f32x4 c = sum4(m, (qk_heads + g) * hd + d);
-          uint16_t* vp = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * hd + ((slot >> 3) * hd + d) * 8 + (slot & 7);
-          for (int e = 0; e < 4; ++e) vp[8 * e] = (uint16_t)f32_to_bf16(c[e]);
-        }
+      const f32x4 lo = sum4(m, h * hd + j), hi = sum4(m, h * hd + half + j);
+      const u32x4 c4 = ld16(csr + j), s4 = ld16(csr + half + j);
+      float rl[4], rh[4];
+      for (int e = 0; e < 4; ++e) {
+        const float c = __uint_as_float(c4[e]), sn = __uint_as_float(s4[e]);
+        rl[e] = lo[e] * c - hi[e] * sn;
+        rh[e] = hi[e] * c + lo[e] * sn;
       }
+      uint16_t* dst;
+      if (h < a.nq) {
+        dst = reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + h * hd;
+      } else {
+        const int slotm = a.tok_slot[m];
+        dst = a.k_pool + (((size_t)(slotm >> 4) * a.nkv + (h - a.nq)) * 16 + (slotm & 15)) * hd;
+      }
+      st8(dst + j, u32x2{pack_bf16x2(rl[0], rl[1]), pack_bf16x2(rl[2], rl[3])});
+      st8(dst + half + j, u32x2{pack_bf16x2(rh[0], rh[1]), pack_bf16x2(rh[2], rh[3])});
+      return;
     }
+    const int dblocks = hd / 32;
+    const int item = (b - a.M * qk_wgs) * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int rb = item / (a.nkv * dblocks), rem = item - rb * (a.nkv * dblocks);
+    const int g = rem / dblocks, d = 32 * (rem - g * dblocks) + 4 * (lane >> 3);
+    const int m = 8 * rb + (lane & 7);
+    if (m >= a.M) return;
+    const f32x4 c = sum4(m, (qk_heads + g) * hd + d);
+    const int slotm = a.tok_slot[m], slot = slotm & 15;
+    uint16_t* vp = a.v_pool + ((size_t)(slotm >> 4) * a.nkv + g) * 16 * hd + ((slot >> 3) * hd + d) * 8 + (slot & 7);
+    for (int e = 0; e < 4; ++e) vp[8 * e] = (uint16_t)f32_to_bf16(c[e]);
     return;
   }
   const int64_t nvec = (int64_t)a.M * a.N / 4;
@@ -761,10 +773,10 @@ constexpr int kReduceWgs = 1024;
 template <int EPI, int KS>
 void launch_reduce_ks(hipStream_t s, const GemmArgs& a, const float* partial) {
   if (EPI == GEMM_QKV_ROPE) {
-    const int row_units = (a.nq + a.nkv) * (a.hd / 8) + a.nkv * (a.hd / 4);
-    const int gx = (row_units + 255) / 256;
-    const int rows_per_wg = (a.M * gx + kReduceWgs - 1) / kReduceWgs;
-    splitk_reduce_kernel<EPI, KS><<<dim3(gx, (a.M + rows_per_wg - 1) / rows_per_wg), 256, 0, s>>>(a, partial);
+    // q/k rows, then V wave items (kv head, 32 dimensions, 8 rows), 4 per workgroup
+    const int qk_units = (a.nq + a.nkv) * (a.hd / 8);
+    const int v_items = a.nkv * (a.hd / 32) * ((a.M + 7) / 8);
+    splitk_reduce_kernel<EPI, KS><<<a.M * ((qk_units + 255) / 256) + (v_items + 3) / 4, 256, 0, s>>>(a, partial);
   } else {
     const int64_t wgs = ((int64_t)a.M * a.N / 4 + 255) / 256;
     const int64_t per = (wgs + kReduceWgs - 1) / kReduceWgs;
