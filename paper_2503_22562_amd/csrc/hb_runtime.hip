@@ -583,7 +583,10 @@ hb_status hb_profile(hb_layer* L, const int32_t* chunk_sizes, int32_t n_chunk, c
       }
       if (st != HB_OK) break;
       if (hipStreamSynchronize(L->stream) != hipSuccess) { st = fail(HB_ERR_HIP, "profiler sync failed"); break; }
-      for (int i = 0; i < iters; ++i) hipEventElapsedTime(&lat[i], ev[2 * i], ev[2 * i + 1]);
+      for (int i = 0; i < iters && st == HB_OK; ++i)
+        if (hipEventElapsedTime(&lat[i], ev[2 * i], ev[2 * i + 1]) != hipSuccess)
+          st = fail(HB_ERR_HIP, "hipEventElapsedTime failed");
+      if (st != HB_OK) break;
       std::vector<float> sorted = lat;
       std::sort(sorted.begin(), sorted.end());
       auto pct = [&](double q) { return sorted[std::min<size_t>(sorted.size() - 1, (size_t)(q * (sorted.size() - 1) + 0.5))]; };
