@@ -49,33 +49,30 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // Online softmax of one column over the N raw scores (q.k) a lane holds for
 // a key step, in log2 units (sc = log2(e)/sqrt(hd)). The running maximum m
-// only moves when some column's step maximum exceeds it by more than
-// RESCALE_SLACK; otherwise the weights 2^(s*sc - m) may reach
-// 2^RESCALE_SLACK, which fp32 accumulation and bf16 weights carry without
-// loss. The result is exact either way (O, l and m change together), and the
-// O rescale -- a read-modify-write of every accumulator -- is mostly skipped.
+// only moves when the weights 2^(s*sc - m) of some lane add up to more than
+// 2^RESCALE_SLACK (so whenever a score exceeds m by more than the slack);
+// below that the weights, at most 2^RESCALE_SLACK, are carried without loss
+// by fp32 accumulation and bf16 weights. The result is exact either way (O,
+// l and m change together), and the O rescale -- a read-modify-write of
+// every accumulator -- is mostly skipped.
 constexpr float RESCALE_SLACK = 8.0f;
+constexpr float kRescaleSum = 256.0f;  // 2^RESCALE_SLACK
 
 // Common case: the weights against the current running maximum and their
-// sum. No cross-lane step maximum is needed: it returns (wave-uniform)
-// whether any weight's exponent exceeds the slack, and then the caller runs
-// softmax_rescale, which recomputes them.
+// sum. No step maximum is formed: the weights are non-negative, so a lane's
+// sum bounds each of its weights, and the step is accepted (wave-uniform)
+// when every lane's sum is at most 2^RESCALE_SLACK. Otherwise (some weight
+// may exceed the slack; rarely, several large ones only add up past it) the
+// caller runs softmax_rescale, which recomputes them exactly.
 template <int N>
 __device__ __forceinline__ bool softmax_fast(const float (&sv)[N], float sc, float m, float& ps, float (&p)[N]) {
-  float t[N];
-#pragma unroll
-  for (int i = 0; i < N; ++i) t[i] = fmaf(sv[i], sc, -m);  // -inf for masked keys
-  float mx = t[0];
-#pragma unroll
-  for (int i = 1; i < N; ++i) mx = fmaxf(mx, t[i]);
-  const bool rescale = __any(mx > RESCALE_SLACK);
   ps = 0.f;
 #pragma unroll
   for (int i = 0; i < N; ++i) {
-    p[i] = __builtin_amdgcn_exp2f(t[i]);  // no denormal results needed
+    p[i] = __builtin_amdgcn_exp2f(fmaf(sv[i], sc, -m));  // 0 for masked keys; no denormal results needed
     ps += p[i];
   }
-  return rescale;
+  return __any(!(ps <= kRescaleSum));
 }
 
 // Rare case: the column's exact step maximum (across the four lanes that
