@@ -271,3 +271,48 @@ def test_every_gemm_tile_shape(hb, monkeypatch, tile, ksplit):
     assert_parity(h2, st["h2"], "h2")
     m = oracle.bf16_bits_to_f64(bf16_bits(dl.stage(H.HB_STAGE_MLP, T)))
     assert_stage(m, st["m"], "silu(gate)*up")
+
+
+def test_back_to_back_iterations_match_one_at_a_time(hb):
+    """Iterations enqueued back to back, with no host synchronisation between
+    them, through the ring of metadata slots (more iterations than slots,
+    metadata of different sizes; two batches' metadata exceed a slot's first
+    allocation, so its host and device buffers grow while earlier iterations
+    are in flight) give bit-identical outputs to the same iterations run one
+    at a time with a synchronisation after each."""
+    import torch
+    from paper_2503_22562_amd.harness import DeviceLayer, to_device_bf16
+    shape = TINY
+    nb = 70000
+    lens_list = [
+        [(64, 128)] + [(1, 256)] * 8,
+        [(1, 7), (1, 300), (37, 21)],
+        [(1, 16000)] * 64,            # ~100k int32 of metadata
+        [(100, 0), (1, 15)],
+        [(5, 3)],
+        [(300, 1200), (1, 2000)],
+        [(1, 9000)] * 96,             # again past the first allocation
+        [(16, 16)],
+        [(1, 0)],
+        [(64, 128)] + [(1, 256)] * 8,
+    ]
+    batches = [make_batch(shape, lens, seed=900 + i, num_blocks=nb) for i, lens in enumerate(lens_list)]
+    w = make_weights(shape)
+    dl = DeviceLayer(shape, w, nb, max(b.n_tokens for b in batches), max(len(b.requests) for b in batches))
+    xs = [to_device_bf16(b.x_in()) for b in batches]
+
+    def reset_pool():
+        dl.k_pool.view(torch.int16).fill_(0x3C00)  # bf16 2^-7
+        dl.v_pool.view(torch.int16).fill_(0x3C00)
+
+    reset_pool()
+    ys = [dl.run(_reqs(b), x) for b, x in zip(batches, xs)]
+    torch.cuda.synchronize()
+    got = [y.cpu().numpy() for y in ys]
+    reset_pool()
+    for i, (b, x) in enumerate(zip(batches, xs)):
+        y = dl.run(_reqs(b), x)
+        torch.cuda.synchronize()
+        ref = y.cpu().numpy()
+        assert np.all(np.isfinite(ref)), f"batch {i}"
+        assert np.array_equal(got[i].view(np.uint32), ref.view(np.uint32)), f"batch {i} differs when enqueued back to back"
