@@ -180,13 +180,88 @@ typedef struct {
  * and its input with seeded pseudo-random bf16, run `warmup` untimed
  * iterations, then `iters` iterations each preceded by a write of a 512 MiB
  * buffer (so no data stays in the 256 MB Infinity Cache) and timed with HIP
- * events. out[m * n_chunk + c] receives the cell. Synchronous. Overwrites the
+ * events; each timed iteration is planned and its metadata uploaded before
+ * its start event, so the interval holds the layer's kernels alone.
+ * out[m * n_chunk + c] receives the cell. Synchronous. Overwrites the
  * pool blocks it uses (an offline step). Errors: HB_ERR_INVALID (null
  * pointer, a batch that does not fit the pool or the layer's capacity,
  * iters < 1), HB_ERR_OOM, HB_ERR_HIP. */
 hb_status hb_profile(hb_layer* layer, const int32_t* chunk_sizes, int32_t n_chunk,
                      const hb_decode_mix* mixes, int32_t n_mix, int32_t warmup, int32_t iters,
                      uint64_t seed, hb_profile_cell* out);
+
+/* Latency of given batches, timed as hb_profile times its cells: for each
+ * batch, `warmup` untimed iterations, then `iters` iterations each after a
+ * write of a 512 MiB buffer, each planned and its metadata uploaded before
+ * the start event, so an interval holds the layer's kernels alone. The
+ * caller supplies each batch's inputs, outputs and block tables (and the
+ * pool contents); the iterations write the batch's new K/V as
+ * hb_run_iteration does. out[b] receives batch b's cell. Synchronous.
+ * Errors: those of hb_validate_batch for any batch (before anything runs),
+ * HB_ERR_INVALID (null pointer, an empty batch, iters < 1, warmup < 0),
+ * HB_ERR_OOM, HB_ERR_HIP. */
+hb_status hb_profile_batches(hb_layer* layer, const hb_batch_desc* batches, int32_t n_batches, int32_t warmup,
+                             int32_t iters, hb_profile_cell* out);
+
+/* Iteration latency model: the lightweight predictor of Section 3.1 (step 4)
+ * and Section 3.3, which the paper trains on offline profiles (Section 3.6),
+ * here fitted to hb_profile cells. The predicted latency (ms) of a batch is
+ * sum_i coef[i] * f_i over the features of the batch:
+ *   f_0  1                                   (fixed per-iteration cost)
+ *   f_1  T / 1000, T = sum of chunk_len       (the linear layers run over T tokens)
+ *   f_2  KV bytes attention reads, GB: sum over requests of
+ *        (context_len + chunk_len) * 2 n_kv_heads head_dim * 2 B
+ *   f_3  attention flops against cached context, TFLOP:
+ *        4 n_q_heads head_dim * sum over requests of chunk_len * context_len
+ *   f_4  attention flops within the new tokens (the causal triangle), TFLOP:
+ *        4 n_q_heads head_dim * sum over requests of chunk_len (chunk_len + 1) / 2
+ * (long-context chunk rows run near the matrix-core rate, the triangle of a
+ * fresh chunk much slower per flop, hence two terms).
+ * A request with chunk_len 0 contributes nothing (it is not in the batch).
+ * All coefficients are >= 0, so the prediction never falls as a chunk grows. */
+#define HB_LAT_FEATURES 5
+typedef struct {
+  double coef[HB_LAT_FEATURES];
+  double fit_rel_rms; /* root mean square of (predicted - measured) / measured over the cells */
+  int32_t n_cells;
+} hb_latency_model;
+
+/* Features f_0..f_4 above of a batch (only chunk_len and context_len are read;
+ * block tables may be NULL). Host only. Errors: HB_ERR_INVALID (null pointer,
+ * n_requests < 0, chunk_len < 0 or context_len < 0 in a request). */
+hb_status hb_latency_features(const hb_layer_config* cfg, const hb_request* requests, int32_t n_requests,
+                              double* features);
+
+/* Fit a model to the median latencies of an hb_profile run, given the same
+ * chunk_sizes and mixes that produced cells[n_mix * n_chunk]: non-negative
+ * least squares on relative error (each cell's row scaled by 1 / median), the
+ * exact optimum over every subset of features. Host only. Errors:
+ * HB_ERR_INVALID (null pointer, fewer cells than features, a median that is
+ * not positive and finite). */
+hb_status hb_fit_latency_model(const hb_layer_config* cfg, const int32_t* chunk_sizes, int32_t n_chunk,
+                               const hb_decode_mix* mixes, int32_t n_mix, const hb_profile_cell* cells,
+                               hb_latency_model* out);
+
+/* Predicted latency (ms) of a batch. Host only. Errors as hb_latency_features. */
+hb_status hb_predict_latency(const hb_latency_model* model, const hb_layer_config* cfg,
+                             const hb_request* requests, int32_t n_requests, double* ms);
+
+/* Dynamic chunking (Section 3.3): the slack of the decode queue is the least,
+ * over its requests, of the deadline of the next token (the TBT deadline
+ * equation of Section 3.2, decode_deadlines_ms[i], on the clock of now_ms)
+ * minus now_ms; with no decodes it is unbounded. The chunk is the largest
+ * c in {granularity, 2 granularity, ...} below max_chunk, or max_chunk itself
+ * (the rest of the prompt), whose batch -- one c-token chunk at chunk_context
+ * next to the decodes -- has a predicted latency within the slack (a
+ * prediction equal to the slack fits); 0 when
+ * none fits or max_chunk is 0. *predicted_ms receives the predicted latency of
+ * the chosen batch (decodes only when *chunk is 0). Host only. Errors:
+ * HB_ERR_INVALID (null pointer, n_decode < 0, a negative context,
+ * chunk_context < 0, max_chunk < 0, granularity < 1, a NaN deadline or now_ms). */
+hb_status hb_select_chunk(const hb_latency_model* model, const hb_layer_config* cfg,
+                          const int32_t* decode_contexts, const double* decode_deadlines_ms, int32_t n_decode,
+                          double now_ms, int32_t chunk_context, int32_t max_chunk, int32_t granularity,
+                          int32_t* chunk, double* predicted_ms);
 
 /* Per-kernel timing of hb_run_iteration, for roofline accounting. Every
  * launch of kernel k with bit k of kernel_mask set is bracketed by HIP events

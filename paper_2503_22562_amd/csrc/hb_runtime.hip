@@ -232,12 +232,20 @@ hb_status check_hip(const char* what) {
   return HB_OK;
 }
 
-// Enqueue the whole layer for a planned batch.
-hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
+// A planned batch made ready to launch: GEMM shapes and plans, workspaces
+// sized, metadata uploaded (the layer's stream waits for the copy).
+struct Prepared {
+  GemmArgs gq, go, gu, gd;
+  GemmPlan pq, po, pu, pd;
+  const int32_t* meta = nullptr;
+  int slot = 0;
+};
+
+// Everything of an iteration up to its launches, for the batch in L->plan.
+hb_status prepare_layer(hb_layer* L, const hb_batch_desc* desc, Prepared* pp) {
   const Dims& d = L->d;
   Plan& p = L->plan;
   const int T = p.T;
-  hipStream_t s = L->stream;
   const uint16_t* x_in = static_cast<const uint16_t*>(desc->x_in);
   GemmArgs gq{}, go{}, gu{}, gd{};
   gq.A = L->xn; gq.lda = d.H;
@@ -279,16 +287,28 @@ hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
   hb_status st = ensure_parts(L, p.n_slots);
   if (st == HB_OK) st = ensure_splitk(L, sk);
   if (st != HB_OK) return st;
-  const int32_t* meta = nullptr;
-  int slot = 0;
-  st = stage_upload(L, p.meta.data(), p.meta.size(), &meta, &slot);
-  if (st != HB_OK) return st;
-  // the slot may be refilled once everything enqueued below has run
+  pp->gq = gq; pp->go = go; pp->gu = gu; pp->gd = gd;
+  pp->pq = pq; pp->po = po; pp->pu = pu; pp->pd = pd;
+  return stage_upload(L, p.meta.data(), p.meta.size(), &pp->meta, &pp->slot);
+}
+
+// The launches of a prepared iteration.
+hb_status launch_layer(hb_layer* L, const hb_batch_desc* desc, const Prepared& pp) {
+  // the metadata slot may be refilled once everything enqueued below has run
   struct Consumed {
     hb_layer* L;
     int slot;
     ~Consumed() { (void)stage_consumed(L, slot); }
-  } consumed{L, slot};
+  } consumed{L, pp.slot};
+  const Dims& d = L->d;
+  const Plan& p = L->plan;
+  const int T = p.T;
+  hipStream_t s = L->stream;
+  const uint16_t* x_in = static_cast<const uint16_t*>(desc->x_in);
+  const GemmArgs &gq = pp.gq, &go = pp.go, &gu = pp.gu, &gd = pp.gd;
+  const GemmPlan &pq = pp.pq, &po = pp.po, &pu = pp.pu, &pd = pp.pd;
+  const int32_t* meta = pp.meta;
+  hb_status st = HB_OK;
 
   RopePrep rp{};
   rp.tok_pos = meta + p.off_tok_pos; rp.tok_req = meta + p.off_tok_req;
@@ -335,6 +355,58 @@ hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
   if (st != HB_OK) return st;
   L->last_T = T;
   return check_hip("kernel launch");
+}
+
+// Enqueue the whole layer for the batch in L->plan.
+hb_status enqueue_layer(hb_layer* L, const hb_batch_desc* desc) {
+  Prepared pp;
+  const hb_status st = prepare_layer(L, desc, &pp);
+  if (st != HB_OK) return st;
+  return launch_layer(L, desc, pp);
+}
+
+// Time one batch as the profiler does: `warmup` untimed iterations, then
+// `iters` iterations, each after a write of `flush_bytes` (no data left in
+// the Infinity Cache); the batch is planned and its metadata uploaded before
+// the start event, so the interval holds the kernels alone. Fills the cell.
+hb_status time_batch(hb_layer* L, const hb_batch_desc* desc, int warmup, int iters, void* flush,
+                     int64_t flush_bytes, std::vector<hipEvent_t>& ev, std::vector<float>& lat, hb_profile_cell* cell) {
+  hb_status st = check_batch(L->d, L->pool.num_blocks, desc, &L->marks);
+  if (st != HB_OK) return st;
+  for (int i = 0; i < warmup && st == HB_OK; ++i) st = hb_run_iteration(L, desc);
+  if (st != HB_OK) return st;
+  build_plan(L->d, desc, L->cu_count, &L->plan, L->plan_opt);
+  for (int i = 0; i < iters && st == HB_OK; ++i) {
+    launch_flush(L->stream, flush, flush_bytes, (uint32_t)i);
+    Prepared pp;
+    st = prepare_layer(L, desc, &pp);
+    if (st != HB_OK) break;
+    if (hipEventRecord(ev[2 * i], L->stream) != hipSuccess) st = fail(HB_ERR_HIP, "hipEventRecord failed");
+    const hb_status sl = launch_layer(L, desc, pp);  // also releases the metadata slot
+    if (st == HB_OK) st = sl;
+    if (st == HB_OK && hipEventRecord(ev[2 * i + 1], L->stream) != hipSuccess)
+      st = fail(HB_ERR_HIP, "hipEventRecord failed");
+  }
+  if (st != HB_OK) return st;
+  if (hipStreamSynchronize(L->stream) != hipSuccess) return fail(HB_ERR_HIP, "profiler sync failed");
+  for (int i = 0; i < iters; ++i)
+    if (hipEventElapsedTime(&lat[i], ev[2 * i], ev[2 * i + 1]) != hipSuccess)
+      return fail(HB_ERR_HIP, "hipEventElapsedTime failed");
+  std::vector<float> sorted(lat.begin(), lat.begin() + iters);
+  std::sort(sorted.begin(), sorted.end());
+  auto pct = [&](double q) { return sorted[std::min<size_t>(sorted.size() - 1, (size_t)(q * (sorted.size() - 1) + 0.5))]; };
+  cell->median_ms = pct(0.5);
+  cell->p10_ms = pct(0.1);
+  cell->p90_ms = pct(0.9);
+  double flops, bytes;
+  iteration_work(L->d, desc->requests, desc->n_requests, &flops, &bytes);
+  int64_t T = 0;
+  for (int r = 0; r < desc->n_requests; ++r) T += desc->requests[r].chunk_len;
+  const double sec = cell->median_ms * 1e-3;
+  cell->tokens_per_s = (float)(T / sec);
+  cell->hbm_frac = (float)(bytes / sec / kPeakHbm);
+  cell->mfma_frac = (float)(flops / sec / kPeakBf16);
+  return HB_OK;
 }
 
 // splitmix64 stream for the profiler's host-side draws
@@ -573,35 +645,41 @@ hb_status hb_profile(hb_layer* L, const int32_t* chunk_sizes, int32_t n_chunk, c
       launch_fill_blocks(L->stream, blocks_dev, used, d.nkv, d.hd, static_cast<uint16_t*>(L->pool.k_pool),
                          static_cast<uint16_t*>(L->pool.v_pool), seed + (uint64_t)used);
       hb_batch_desc desc{(int32_t)reqs.size(), reqs.data(), x_in, x_out, HB_OUT_F32};
-      for (int i = 0; i < warmup && st == HB_OK; ++i) st = hb_run_iteration(L, &desc);
-      for (int i = 0; i < iters && st == HB_OK; ++i) {
-        launch_flush(L->stream, flush, flush_bytes, (uint32_t)i);
-        if (hipEventRecord(ev[2 * i], L->stream) != hipSuccess) st = fail(HB_ERR_HIP, "hipEventRecord failed");
-        if (st == HB_OK) st = hb_run_iteration(L, &desc);
-        if (st == HB_OK && hipEventRecord(ev[2 * i + 1], L->stream) != hipSuccess)
-          st = fail(HB_ERR_HIP, "hipEventRecord failed");
-      }
-      if (st != HB_OK) break;
-      if (hipStreamSynchronize(L->stream) != hipSuccess) { st = fail(HB_ERR_HIP, "profiler sync failed"); break; }
-      for (int i = 0; i < iters && st == HB_OK; ++i)
-        if (hipEventElapsedTime(&lat[i], ev[2 * i], ev[2 * i + 1]) != hipSuccess)
-          st = fail(HB_ERR_HIP, "hipEventElapsedTime failed");
-      if (st != HB_OK) break;
-      std::vector<float> sorted = lat;
-      std::sort(sorted.begin(), sorted.end());
-      auto pct = [&](double q) { return sorted[std::min<size_t>(sorted.size() - 1, (size_t)(q * (sorted.size() - 1) + 0.5))]; };
-      hb_profile_cell& cell = out[mi * n_chunk + ci];
-      cell.median_ms = pct(0.5);
-      cell.p10_ms = pct(0.1);
-      cell.p90_ms = pct(0.9);
-      double flops, bytes;
-      iteration_work(d, reqs.data(), (int)reqs.size(), &flops, &bytes);
-      const double sec = cell.median_ms * 1e-3;
-      cell.tokens_per_s = (float)((c + mx.n_decode) / sec);
-      cell.hbm_frac = (float)(bytes / sec / kPeakHbm);
-      cell.mfma_frac = (float)(flops / sec / kPeakBf16);
+      st = time_batch(L, &desc, warmup, iters, flush, flush_bytes, ev, lat, &out[mi * n_chunk + ci]);
     }
   }
+  cleanup();
+  return st;
+}
+
+hb_status hb_profile_batches(hb_layer* L, const hb_batch_desc* batches, int32_t n_batches, int32_t warmup,
+                             int32_t iters, hb_profile_cell* out) {
+  if (!L || !out || n_batches < 0 || (n_batches > 0 && !batches)) return fail(HB_ERR_INVALID, "null argument");
+  if (iters < 1 || warmup < 0) return fail(HB_ERR_INVALID, "iters < 1 or warmup < 0");
+  for (int b = 0; b < n_batches; ++b) {
+    const hb_status st = check_batch(L->d, L->pool.num_blocks, &batches[b], &L->marks);
+    if (st != HB_OK) return st;
+    if (batches[b].n_requests == 0) return fail(HB_ERR_INVALID, "batch %d is empty", b);
+  }
+  const int64_t flush_bytes = (int64_t)512 << 20;
+  void* flush = nullptr;
+  std::vector<hipEvent_t> ev(2 * (size_t)iters, nullptr);
+  std::vector<float> lat(iters);
+  auto cleanup = [&]() {
+    (void)hipStreamSynchronize(L->stream);
+    if (flush) (void)hipFree(flush);
+    for (hipEvent_t e : ev)
+      if (e) (void)hipEventDestroy(e);
+  };
+  if (hipMalloc(&flush, flush_bytes) != hipSuccess) {
+    cleanup();
+    return fail(HB_ERR_OOM, "profiler flush buffer");
+  }
+  for (auto& e : ev)
+    if (hipEventCreate(&e) != hipSuccess) { cleanup(); return fail(HB_ERR_HIP, "hipEventCreate failed"); }
+  hb_status st = HB_OK;
+  for (int b = 0; b < n_batches && st == HB_OK; ++b)
+    st = time_batch(L, &batches[b], warmup, iters, flush, flush_bytes, ev, lat, &out[b]);
   cleanup();
   return st;
 }

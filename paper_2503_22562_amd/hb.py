@@ -20,8 +20,9 @@ HB_OUT_F32, HB_OUT_BF16 = 0, 1
 HB_STAGE_Q, HB_STAGE_ATTN, HB_STAGE_H2, HB_STAGE_MLP = range(4)
 
 EXPORTED = ("hb_create_layer", "hb_destroy_layer", "hb_append_kv", "hb_run_iteration", "hb_validate_batch",
-            "hb_profile", "hb_set_kernel_timing", "hb_kernel_times", "hb_kernel_name", "hb_layer_stage",
-            "hb_last_error")
+            "hb_profile", "hb_profile_batches", "hb_latency_features", "hb_fit_latency_model", "hb_predict_latency", "hb_select_chunk",
+            "hb_set_kernel_timing", "hb_kernel_times", "hb_kernel_name", "hb_layer_stage", "hb_last_error")
+HB_LAT_FEATURES = 5
 
 
 class hb_layer_config(C.Structure):
@@ -55,6 +56,10 @@ class hb_decode_mix(C.Structure):
 
 class hb_profile_cell(C.Structure):
     _fields_ = [(n, C.c_float) for n in ("median_ms", "p10_ms", "p90_ms", "tokens_per_s", "hbm_frac", "mfma_frac")]
+
+
+class hb_latency_model(C.Structure):
+    _fields_ = [("coef", C.c_double * HB_LAT_FEATURES), ("fit_rel_rms", C.c_double), ("n_cells", C.c_int32)]
 
 
 class HBError(RuntimeError):
@@ -93,6 +98,23 @@ def load() -> C.CDLL:
     lib.hb_profile.argtypes = [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.POINTER(hb_decode_mix), C.c_int32,
                                C.c_int32, C.c_int32, C.c_uint64, C.POINTER(hb_profile_cell)]
     lib.hb_profile.restype = st
+    lib.hb_profile_batches.argtypes = [C.c_void_p, C.POINTER(hb_batch_desc), C.c_int32, C.c_int32, C.c_int32,
+                                       C.POINTER(hb_profile_cell)]
+    lib.hb_profile_batches.restype = st
+    lib.hb_latency_features.argtypes = [C.POINTER(hb_layer_config), C.POINTER(hb_request), C.c_int32,
+                                        C.POINTER(C.c_double)]
+    lib.hb_latency_features.restype = st
+    lib.hb_fit_latency_model.argtypes = [C.POINTER(hb_layer_config), C.POINTER(C.c_int32), C.c_int32,
+                                         C.POINTER(hb_decode_mix), C.c_int32, C.POINTER(hb_profile_cell),
+                                         C.POINTER(hb_latency_model)]
+    lib.hb_fit_latency_model.restype = st
+    lib.hb_predict_latency.argtypes = [C.POINTER(hb_latency_model), C.POINTER(hb_layer_config), C.POINTER(hb_request),
+                                       C.c_int32, C.POINTER(C.c_double)]
+    lib.hb_predict_latency.restype = st
+    lib.hb_select_chunk.argtypes = [C.POINTER(hb_latency_model), C.POINTER(hb_layer_config), C.POINTER(C.c_int32),
+                                    C.POINTER(C.c_double), C.c_int32, C.c_double, C.c_int32, C.c_int32, C.c_int32,
+                                    C.POINTER(C.c_int32), C.POINTER(C.c_double)]
+    lib.hb_select_chunk.restype = st
     lib.hb_set_kernel_timing.argtypes = [C.c_void_p, C.c_uint32]
     lib.hb_set_kernel_timing.restype = st
     lib.hb_kernel_times.argtypes = [C.c_void_p, C.POINTER(C.c_double), C.POINTER(C.c_int64), C.c_int32]
@@ -216,6 +238,85 @@ def hb_profile(layer: Layer, chunk_sizes: Sequence[int], mixes: Sequence[Tuple[S
             cell = out[i * len(cs) + j]
             res[i, j] = tuple(getattr(cell, n) for n in names)
     return res
+
+
+def hb_profile_batches(layer: Layer, batches, warmup: int = 3, iters: int = 15) -> np.ndarray:
+    """batches: (requests, x_in, x_out) each, requests as for hb_run_iteration.
+    Returns a structured array [n_batches] of profile cells."""
+    descs = (hb_batch_desc * max(1, len(batches)))()
+    keep = []
+    for i, (reqs, x_in, x_out) in enumerate(batches):
+        import torch
+        out_dtype = HB_OUT_F32 if x_out.dtype == torch.float32 else HB_OUT_BF16
+        d, k = _desc(reqs, _ptr(x_in), _ptr(x_out), out_dtype)
+        descs[i] = d
+        keep.append(k)
+    out = (hb_profile_cell * max(1, len(batches)))()
+    _check(load().hb_profile_batches(layer.handle, descs, len(batches), int(warmup), int(iters), out))
+    names = [f[0] for f in hb_profile_cell._fields_]
+    res = np.zeros(len(batches), dtype=[(n, np.float64) for n in names])
+    for i in range(len(batches)):
+        res[i] = tuple(getattr(out[i], n) for n in names)
+    return res
+
+
+def _requests_only(requests: Sequence[Tuple[int, int]]):
+    """hb_request array of (chunk_len, context_len) pairs without block tables."""
+    arr = (hb_request * max(1, len(requests)))()
+    for i, r in enumerate(requests):
+        arr[i] = hb_request(int(r[0]), int(r[1]), None, 0)
+    return arr
+
+
+def _mix_array(mixes: Sequence[Tuple[Sequence[int], int]]):
+    ctxs = [_i32(m[0]) for m in mixes]
+    marr = (hb_decode_mix * len(mixes))()
+    for i, (c, (_, cc)) in enumerate(zip(ctxs, mixes)):
+        marr[i] = hb_decode_mix(len(c), c.ctypes.data_as(C.POINTER(C.c_int32)), int(cc))
+    return marr, ctxs
+
+
+def hb_latency_features(cfg: hb_layer_config, requests: Sequence[Tuple[int, int]]) -> np.ndarray:
+    """requests: (chunk_len, context_len) per request."""
+    f = (C.c_double * HB_LAT_FEATURES)()
+    _check(load().hb_latency_features(C.byref(cfg), _requests_only(requests), len(requests), f))
+    return np.array(f[:], dtype=np.float64)
+
+
+def hb_fit_latency_model(cfg: hb_layer_config, chunk_sizes: Sequence[int],
+                         mixes: Sequence[Tuple[Sequence[int], int]], median_ms) -> hb_latency_model:
+    """median_ms[n_mix][n_chunk]: the cells' medians (hb_profile's "median_ms")."""
+    cs = _i32(chunk_sizes)
+    marr, keep = _mix_array(mixes)
+    med = np.asarray(median_ms, dtype=np.float64).reshape(len(mixes), len(cs))
+    cells = (hb_profile_cell * med.size)()
+    for i in range(len(mixes)):
+        for j in range(len(cs)):
+            cells[i * len(cs) + j].median_ms = float(med[i, j])
+    model = hb_latency_model()
+    _check(load().hb_fit_latency_model(C.byref(cfg), cs.ctypes.data_as(C.POINTER(C.c_int32)), len(cs), marr,
+                                       len(mixes), cells, C.byref(model)))
+    return model
+
+
+def hb_predict_latency(model: hb_latency_model, cfg: hb_layer_config, requests: Sequence[Tuple[int, int]]) -> float:
+    ms = C.c_double()
+    _check(load().hb_predict_latency(C.byref(model), C.byref(cfg), _requests_only(requests), len(requests),
+                                     C.byref(ms)))
+    return ms.value
+
+
+def hb_select_chunk(model: hb_latency_model, cfg: hb_layer_config, decode_contexts: Sequence[int],
+                    decode_deadlines_ms: Sequence[float], now_ms: float, chunk_context: int, max_chunk: int,
+                    granularity: int) -> Tuple[int, float]:
+    ctx = _i32(decode_contexts)
+    dl = np.ascontiguousarray(decode_deadlines_ms, dtype=np.float64)
+    chunk, ms = C.c_int32(), C.c_double()
+    _check(load().hb_select_chunk(C.byref(model), C.byref(cfg), ctx.ctypes.data_as(C.POINTER(C.c_int32)),
+                                  dl.ctypes.data_as(C.POINTER(C.c_double)), len(ctx), float(now_ms),
+                                  int(chunk_context), int(max_chunk), int(granularity), C.byref(chunk),
+                                  C.byref(ms)))
+    return chunk.value, ms.value
 
 
 def hb_set_kernel_timing(layer: Layer, kernels) -> None:

@@ -86,3 +86,67 @@ def test_latency_profile_monotone_in_chunk_size(hb):
 @pytest.mark.timeout(900)
 def test_llama70b_chunk2048_plus_32_decodes(hb):
     _check_batch(llama70b_batch(), max_T=2080, max_R=64, n_dec=4)
+
+
+def _fill_pool_random(dl, seed=5):
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    for t in (dl.k_pool, dl.v_pool):
+        flat = t.view(-1)
+        for s in range(0, flat.numel(), 1 << 28):
+            n = min(1 << 28, flat.numel() - s)
+            flat[s:s + n].copy_(torch.randn(n, device="cuda", generator=g).to(torch.bfloat16))
+
+
+def test_latency_model_predicts_off_grid_batches_and_selects_chunks(hb):
+    """The latency model fitted to profile cells (the sweep grid plus chunks
+    after a 4096-token context) predicts batches off that grid -- several
+    chunks with 256 decodes, decode-only, long-context chunks -- within 15%
+    on average and 25% at worst (kernel time, cold cache, both sides timed
+    the same way); and a chunk the selector picks for a given slack runs
+    within that slack (10% allowance for the model's error)."""
+    import torch
+    from paper_2503_22562_amd import hb as H
+    from paper_2503_22562_amd.harness import to_device_bf16
+    from hb_workloads import make_batch
+    dl, _, _ = _device_layer(LLAMA3_8B, 4096, 512)
+    _fill_pool_random(dl)
+    mixes = [(sweep_decode_contexts(n), 0) for n in SWEEP_DECODES] + [([], 4096), (sweep_decode_contexts(64), 4096)]
+    prof = H.hb_profile(dl.layer, SWEEP_CHUNKS, mixes, warmup=3, iters=15, seed=1)
+    model = H.hb_fit_latency_model(dl.cfg, SWEEP_CHUNKS, mixes, prof["median_ms"])
+    print("coef", np.round(list(model.coef), 4), "fit rel rms", round(model.fit_rel_rms, 4))
+    rng = np.random.default_rng(21)
+    shape = LLAMA3_8B
+    vals = [llama8b_batch(), multi_batch(), sweep_batch(384, 64),
+            make_batch(shape, [(1, int(c)) for c in rng.integers(256, 8192, 200)], 41),
+            make_batch(shape, [(768, 6000)] + [(1, int(c)) for c in rng.integers(512, 4096, 100)], 42),
+            make_batch(shape, [(2048, 8192)], 43)]
+    keep, batches = [], []
+    for b in vals:
+        x = to_device_bf16(b.x_in())
+        y = torch.empty((b.n_tokens, shape.hidden), dtype=torch.float32, device="cuda")
+        keep.append((x, y))
+        batches.append(([(q.chunk_len, q.context_len, q.block_table) for q in b.requests], x, y))
+    cells = H.hb_profile_batches(dl.layer, batches, warmup=3, iters=15)
+    errs = []
+    for b, cell in zip(vals, cells):
+        pred = H.hb_predict_latency(model, dl.cfg, [(q.chunk_len, q.context_len) for q in b.requests])
+        errs.append(pred / cell["median_ms"] - 1)
+        print(f"T={b.n_tokens:5d} requests={len(b.requests):3d} measured {cell['median_ms']:.4f} "
+              f"predicted {pred:.4f} ({100 * errs[-1]:+.1f}%)")
+    errs = np.abs(errs)
+    assert errs.mean() <= 0.15 and errs.max() <= 0.25, errs
+
+    # dynamic chunking: 64 decodes, the chunk of a prompt at context 2048
+    ctx = [int(c) for c in rng.integers(512, 4096, 64)]
+    for slack in (0.45, 0.6, 0.9):
+        c, pred = H.hb_select_chunk(model, dl.cfg, ctx, [100.0 + slack] * 64, 100.0, 2048, 4096, 32)
+        assert c > 0, f"slack {slack} ms admits no chunk"
+        b = make_batch(shape, [(c, 2048)] + [(1, x) for x in ctx], 50)
+        x = to_device_bf16(b.x_in())
+        y = torch.empty((b.n_tokens, shape.hidden), dtype=torch.float32, device="cuda")
+        meas = H.hb_profile_batches(dl.layer, [([(q.chunk_len, q.context_len, q.block_table) for q in b.requests],
+                                                 x, y)], warmup=3, iters=15)[0]["median_ms"]
+        print(f"slack {slack} ms: chunk {c}, predicted {pred:.4f}, measured {meas:.4f}")
+        assert meas <= slack * 1.10
