@@ -173,6 +173,62 @@ def regime(hb, dl, batch, shape, x_dev, y_dev, steps):
     return out
 
 
+def fit_and_validate_latency_model(hb, dl, shape, mixes, median_ms, iters):
+    """Fit the iteration latency model (hb_fit_latency_model) to the latency
+    profile's cells plus cells whose chunk follows a 4096-token context, then
+    time batches off that grid with hb_profile_batches (the same kernel-only,
+    cold-cache timing) against the model's predictions, and let the chunk
+    selector pick chunks for three slacks next to 64 decodes."""
+    import torch
+    from hb_workloads import (SWEEP_CHUNKS, llama8b_batch, make_batch, multi_batch, sweep_batch,
+                              sweep_decode_contexts)
+    from paper_2503_22562_amd.harness import to_device_bf16
+    extra = [([], 4096), (sweep_decode_contexts(64), 4096)]
+    prof2 = hb.hb_profile(dl.layer, SWEEP_CHUNKS, extra, warmup=3, iters=iters, seed=2)
+    model = hb.hb_fit_latency_model(dl.cfg, SWEEP_CHUNKS, list(mixes) + extra,
+                                    np.vstack([median_ms, prof2["median_ms"]]))
+    rng = np.random.default_rng(21)
+
+    def timed(batches):
+        keep, args = [], []
+        for b in batches:
+            x = to_device_bf16(b.x_in())
+            y = torch.empty((b.n_tokens, shape.hidden), dtype=torch.float32, device="cuda")
+            keep.append((x, y))
+            args.append(([(q.chunk_len, q.context_len, q.block_table) for q in b.requests], x, y))
+        return hb.hb_profile_batches(dl.layer, args, warmup=3, iters=iters)["median_ms"]
+
+    vals = {"chunk 512 at 3431 + 64 decodes (the bench batch)": llama8b_batch(),
+            "4 chunks + 256 decodes (multi-request batch)": multi_batch(),
+            "chunk 384 + 64 decodes": sweep_batch(384, 64),
+            "200 decodes, contexts U{256..8192}": make_batch(shape, [(1, int(c)) for c in rng.integers(256, 8192, 200)], 41),
+            "chunk 768 at 6000 + 100 decodes": make_batch(
+                shape, [(768, 6000)] + [(1, int(c)) for c in rng.integers(512, 4096, 100)], 42),
+            "chunk 2048 at 8192": make_batch(shape, [(2048, 8192)], 43)}
+    meas = timed(vals.values())
+    validation = []
+    for (name, b), m in zip(vals.items(), meas):
+        p = hb.hb_predict_latency(model, dl.cfg, [(q.chunk_len, q.context_len) for q in b.requests])
+        validation.append({"batch": name, "measured_ms": round(float(m), 4), "predicted_ms": round(p, 4)})
+    errs = [abs(v["predicted_ms"] / v["measured_ms"] - 1) for v in validation]
+    ctx = [int(c) for c in rng.integers(512, 4096, 64)]
+    picks, sel_batches = [], []
+    for slack in (0.45, 0.6, 0.9):
+        c, p = hb.hb_select_chunk(model, dl.cfg, ctx, [100.0 + slack] * 64, 100.0, 2048, 4096, 32)
+        picks.append((slack, c, p))
+        sel_batches.append(make_batch(shape, [(max(c, 1), 2048)] + [(1, x) for x in ctx], 50))
+    sel_meas = timed(sel_batches)
+    return {"features": ["1", "T/1e3", "KV GB read", "attention TFLOP vs cached context",
+                         "attention TFLOP within new tokens"],
+            "coef_ms": [round(c, 5) for c in model.coef], "fit_cells": model.n_cells,
+            "fit_rel_rms": round(model.fit_rel_rms, 4), "validation": validation,
+            "validation_mape": round(float(np.mean(errs)), 4), "validation_max_err": round(float(np.max(errs)), 4),
+            "selector": [{"decodes": 64, "chunk_context": 2048, "slack_ms": s, "chunk": c,
+                          "predicted_ms": round(p, 4), "measured_ms": round(float(m), 4)}
+                         for (s, c, p), m in zip(picks, sel_meas)],
+            "timing": "kernel time per iteration, 512 MiB write before each (hb_profile / hb_profile_batches)"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -340,6 +396,11 @@ def main() -> int:
                    "mfma_frac": np.round(prof["mfma_frac"], 3).tolist(),
                    "monotone_in_chunk": bool(mono), "cache": "512 MiB flush before each timed iteration"}
 
+    latency_model = None
+    if not a.no_profile:
+        log("bench: latency model (fit, off-grid validation, chunk selection)")
+        latency_model = fit_and_validate_latency_model(hb, dl, shape, mixes, prof["median_ms"], a.profile_iters)
+
     cpu = None
     if not a.no_cpu_baseline:
         log("bench: CPU oracle baseline")
@@ -381,6 +442,7 @@ def main() -> int:
         "regimes": regimes,
         "regimes_note": "per-kernel averages with every launch bracketed by events; algorithmic work as for roofline",
         "latency_profile": profile,
+        "latency_model": latency_model,
     }
     print(json.dumps(out), flush=True)
     return 0
