@@ -229,16 +229,74 @@ def fit_and_validate_latency_model(hb, dl, shape, mixes, median_ms, iters):
             "timing": "kernel time per iteration, 512 MiB write before each (hb_profile / hb_profile_batches)"}
 
 
+def model_iteration(hb, torch, shape, batch_lens, seed, n_layers=32, vocab=128256, steps=20, warmup=3):
+    """Whole-model iteration (hb_run_model): n_layers decoder layers of the
+    given shape between a token embedding and the LM head, on the same
+    request mix as the layer bench. Weights and cached K/V are drawn on the
+    device (seeded; they only need realistic sizes and finite values here);
+    each layer has its own pool, sized to the blocks the batch uses."""
+    from hb_workloads import make_batch
+    need = sum(-(-(c + x) // 16) for c, x in batch_lens)
+    nb = need + 64
+    b = make_batch(shape, batch_lens, seed, num_blocks=nb)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    H, F, nq, nkv, hd = shape.hidden, shape.ffn_dim, shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+
+    def randn(rows, cols, std):
+        return (torch.randn((rows, cols), generator=g, device="cuda") * std).to(torch.bfloat16)
+
+    layers, pools = [], []
+    for _ in range(n_layers):
+        layers.append({"w_qkv": randn((nq + 2 * nkv) * hd, H, H ** -0.5), "w_o": randn(H, nq * hd, (nq * hd) ** -0.5),
+                       "w_gate_up": randn(2 * F, H, H ** -0.5), "w_down": randn(H, F, F ** -0.5),
+                       "g_attn": (1 + 0.1 * torch.randn(H, generator=g, device="cuda")).to(torch.bfloat16),
+                       "g_ffn": (1 + 0.1 * torch.randn(H, generator=g, device="cuda")).to(torch.bfloat16)})
+        pools.append((torch.randn((nb, nkv, 16, hd), generator=g, device="cuda", dtype=torch.bfloat16),
+                      torch.randn((nb, nkv, 2, hd, 8), generator=g, device="cuda", dtype=torch.bfloat16)))
+    embed = torch.randn((vocab, H), generator=g, device="cuda", dtype=torch.bfloat16)
+    head = randn(vocab, H, H ** -0.5)
+    g_final = (1 + 0.1 * torch.randn(H, generator=g, device="cuda")).to(torch.bfloat16)
+    cfg = hb.make_config(shape, max(b.n_tokens, 1), max(len(b.requests), 1))
+    model = hb.hb_create_model(cfg, layers, pools, nb, embed, g_final, head)
+    reqs = [(q.chunk_len, q.context_len, q.block_table) for q in b.requests]
+    ids = torch.from_numpy(b.token_ids(vocab)).to("cuda")
+    nxt = torch.empty(len(reqs), dtype=torch.int32, device="cuda")
+    for _ in range(warmup):
+        hb.hb_run_model(model, reqs, ids, nxt)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for i in range(steps):
+        ev[i][0].record(stream)
+        hb.hb_run_model(model, reqs, ids, nxt)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    ts = sorted(s.elapsed_time(e) for s, e in ev)
+    med = ts[len(ts) // 2]
+    T = b.n_tokens
+    weight_gb = (n_layers * (H * (nq + 2 * nkv) * hd + nq * hd * H + 3 * H * F) + vocab * H) * 2 / 1e9
+    del model, layers, pools, embed, head
+    torch.cuda.empty_cache()
+    return {"layers": n_layers, "vocab": vocab, "tokens": T, "requests": len(reqs),
+            "median_ms": round(med, 4), "p10_ms": round(ts[len(ts) // 10], 4),
+            "p90_ms": round(ts[(9 * len(ts)) // 10], 4), "tokens_per_s": round(T / (med * 1e-3), 1),
+            "weights_gb": round(weight_gb, 2),
+            "note": "time between tokens of every decode in the batch = one iteration; "
+                    "compare with the strictest QoS tier's 50 ms"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--profile-iters", type=int, default=15)
     ap.add_argument("--regime-steps", type=int, default=10)
     ap.add_argument("--no-regimes", action="store_true")
+    ap.add_argument("--no-model", action="store_true", help="skip the 32-layer whole-model iteration")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration) and exit")
     a = ap.parse_args()
@@ -401,6 +459,11 @@ def main() -> int:
         log("bench: latency model (fit, off-grid validation, chunk selection)")
         latency_model = fit_and_validate_latency_model(hb, dl, shape, mixes, prof["median_ms"], a.profile_iters)
 
+    model = None
+    if not a.no_model:
+        log("bench: whole-model iteration (32 layers, LM head)")
+        model = model_iteration(hb, torch, shape, [(c, xx) for c, xx, _ in reqs], batch.seed)
+
     cpu = None
     if not a.no_cpu_baseline:
         log("bench: CPU oracle baseline")
@@ -443,6 +506,7 @@ def main() -> int:
         "regimes_note": "per-kernel averages with every launch bracketed by events; algorithmic work as for roofline",
         "latency_profile": profile,
         "latency_model": latency_model,
+        "model_iteration": model,
     }
     print(json.dumps(out), flush=True)
     return 0

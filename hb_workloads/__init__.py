@@ -147,6 +147,20 @@ def make_weights(shape: LayerShape, seed: Optional[int] = None) -> Dict[str, np.
     return out
 
 
+def make_model_weights(shape: LayerShape, n_layers: int, vocab: int, seed: Optional[int] = None) -> Dict:
+    """Random-init weights of an n_layers model: per layer as make_weights
+    (seed 1000 * seed + layer + 1), token embedding ~ N(0,1) (so hidden states
+    start at the layer inputs' N(0,1) scale), LM head ~ N(0, 1/hidden), final
+    RMSNorm gain 1 + 0.1 N(0,1); bf16 bits, rows [vocab][hidden]."""
+    seed = shape.weight_seed if seed is None else seed
+    h = shape.hidden
+    rng = np.random.default_rng([seed, 22])
+    return {"layers": [make_weights(shape, seed=1000 * seed + l + 1) for l in range(n_layers)],
+            "embed": normal_bf16([seed, 20], (vocab, h), 1.0),
+            "lm_head": normal_bf16([seed, 21], (vocab, h), 1.0 / math.sqrt(h)),
+            "g_final": f32_to_bf16_bits((1.0 + 0.1 * rng.standard_normal(size=(h,), dtype=np.float32)))}
+
+
 # ----------------------------------------------------------------------------
 # Batches
 # ----------------------------------------------------------------------------
@@ -184,12 +198,18 @@ class Batch:
         """Token activations ~ N(0,1), bf16 bits [T][hidden]."""
         return normal_bf16([self.seed, 1], (self.n_tokens, self.shape.hidden))
 
-    def prior_kv(self, r: int) -> Tuple[np.ndarray, np.ndarray]:
+    def prior_kv(self, r: int, layer: int = 0) -> Tuple[np.ndarray, np.ndarray]:
         """Synthetic cached K (already rotated) and V for positions [0, ctx) of
-        request r, each ~ N(0,1), bf16 bits [ctx][n_kv][head_dim]."""
+        request r in decoder layer `layer`, each ~ N(0,1), bf16 bits
+        [ctx][n_kv][head_dim]."""
         req = self.requests[r]
         shp = (req.context_len, self.shape.n_kv_heads, self.shape.head_dim)
-        return normal_bf16([self.seed, 2, r, 0], shp), normal_bf16([self.seed, 2, r, 1], shp)
+        key = [self.seed, 2, r] if layer == 0 else [self.seed, 2, r, 100 + layer]
+        return normal_bf16(key + [0], shp), normal_bf16(key + [1], shp)
+
+    def token_ids(self, vocab: int) -> np.ndarray:
+        """Input token ids of the batch rows, uniform over [0, vocab), int32 [T]."""
+        return np.random.default_rng([self.seed, 3]).integers(0, vocab, self.n_tokens).astype(np.int32)
 
 
 def blocks_needed(kv_len: int, block: int = KV_BLOCK) -> int:

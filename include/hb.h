@@ -263,6 +263,57 @@ hb_status hb_select_chunk(const hb_latency_model* model, const hb_layer_config* 
                           double now_ms, int32_t chunk_context, int32_t max_chunk, int32_t granularity,
                           int32_t* chunk, double* predicted_ms);
 
+/* Whole-model iteration: n_layers decoder layers (each an hb_layer with its
+ * own weights and its own paged pool) between a token embedding and a final
+ * RMSNorm + LM head, so the time between tokens of one scheduler iteration
+ * (Section 3.1, steps 5-6) can be set against the TBT targets of the QoS
+ * buckets (evaluation, QoS table: 50 ms for the strictest). Hidden states
+ * pass between layers as bf16; greedy decoding takes the argmax.
+ *   layers  [n_layers] weights as for hb_create_layer
+ *   pools   [n_layers] paged pools, all with the same num_blocks: a request's
+ *           block table names the same blocks in every layer's pool
+ *   embed   device bf16 [vocab][H]; g_final device bf16 [H]; lm_head device
+ *           bf16 [vocab][H]; vocab % 8 == 0
+ * Caller-owned; everything must outlive the model. */
+typedef struct hb_model hb_model; /* opaque, library-owned */
+typedef struct {
+  int32_t n_layers, vocab;
+  const hb_layer_weights* layers;
+  const hb_kv_pool* pools;
+  const void *embed, *g_final, *lm_head;
+} hb_model_desc;
+
+/* Create a model on a HIP stream (all its layers use it). Errors as
+ * hb_create_layer, and HB_ERR_INVALID for n_layers < 1, vocab < 8 or not a
+ * multiple of 8, pools of different sizes, null pointers. *out is NULL on
+ * error. */
+hb_status hb_create_model(const hb_layer_config* cfg, const hb_model_desc* desc, void* hip_stream,
+                          hb_model** out);
+void hb_destroy_model(hb_model* model);
+
+/* Layer `index` of a model (NULL for an index outside [0, n_layers)), owned
+ * by the model: for hb_append_kv into that layer's pool, hb_layer_stage and
+ * the per-kernel timing calls; not to be destroyed by the caller. */
+hb_layer* hb_model_layer(hb_model* model, int32_t index);
+
+/* One model iteration over a hybrid batch: requests as for hb_run_iteration
+ * (their K/V are written into every layer's pool); token_ids device int32
+ * [T] in descriptor order (ids outside [0, vocab) read the nearest embedding
+ * row); for the last row of each request, logits (device fp32
+ * [n_requests][vocab], or NULL to keep them internal) and next_tokens
+ * (device int32 [n_requests]: the lowest index of the largest logit).
+ * Enqueues on the model's stream and returns. Errors: those of
+ * hb_run_iteration, HB_ERR_INVALID for null token_ids / next_tokens or an
+ * empty batch. */
+typedef struct {
+  int32_t n_requests;
+  const hb_request* requests;
+  const int32_t* token_ids;
+  float* logits;
+  int32_t* next_tokens;
+} hb_model_batch;
+hb_status hb_run_model(hb_model* model, const hb_model_batch* batch);
+
 /* Per-kernel timing of hb_run_iteration, for roofline accounting. Every
  * launch of kernel k with bit k of kernel_mask set is bracketed by HIP events
  * on the layer's stream (mask 0 turns timing off; timing one kernel keeps the

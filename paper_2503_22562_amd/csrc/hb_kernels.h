@@ -51,7 +51,7 @@ struct GemmArgs {
   const uint16_t* B; int ldb;
   int M, N, K;
   void* C; int ldc; int c_f32;
-  const void* R; int ldr; int r_f32;
+  const void* R; int ldr; int r_f32;  // GEMM_RESIDUAL: residual added to the product (NULL: none)
   int epi;
   // GEMM_QKV_ROPE only
   const float* rope_cs; const int32_t* tok_slot;
@@ -111,5 +111,10 @@ void launch_fill_blocks(hipStream_t s, const int32_t* blocks, int n, int nkv, in
                         uint16_t* v_pool, uint64_t seed);
 // Overwrite a buffer (evicts earlier data from the Infinity Cache).
 void launch_flush(hipStream_t s, void* buf, int64_t bytes, uint32_t value);
+// out[r][:] = src[clamp(rows[r], 0, n_src - 1)][:] (bf16 rows of H, H % 8 == 0).
+void launch_gather_rows(hipStream_t s, const uint16_t* src, int64_t n_src, const int32_t* rows, int n_rows, int H,
+                        uint16_t* out);
+// out[r] = index of the largest of x[r][0..V) (lowest index on ties).
+void launch_argmax(hipStream_t s, const float* x, int n_rows, int V, int32_t* out);
 
 }  // namespace hb

@@ -165,4 +165,57 @@ void launch_flush(hipStream_t s, void* buf, int64_t bytes, uint32_t value) {
   flush_kernel<<<4096, 256, 0, s>>>(reinterpret_cast<u32x4*>(buf), n, value);
 }
 
+// out[r] = src[rows[r]] for r < n_rows, H bf16 each (H % 8 == 0): token
+// embedding lookup and the selection of each request's last row. One
+// workgroup per row.
+__global__ __launch_bounds__(256) void gather_rows_kernel(const uint16_t* __restrict__ src, int64_t n_src,
+                                                          const int32_t* __restrict__ rows, int H,
+                                                          uint16_t* __restrict__ out) {
+  const int r = blockIdx.x;
+  const int64_t row = min<int64_t>(max(rows[r], 0), n_src - 1);  // ids outside [0, n_src) read the nearest row
+  const u32x4* s4 = reinterpret_cast<const u32x4*>(src + row * H);
+  u32x4* d4 = reinterpret_cast<u32x4*>(out + (int64_t)r * H);
+  for (int v = threadIdx.x; v < H / 8; v += 256) d4[v] = s4[v];
+}
+
+void launch_gather_rows(hipStream_t s, const uint16_t* src, int64_t n_src, const int32_t* rows, int n_rows, int H,
+                        uint16_t* out) {
+  if (n_rows <= 0) return;
+  gather_rows_kernel<<<n_rows, 256, 0, s>>>(src, n_src, rows, H, out);
+}
+
+// Index of the largest of V fp32 values per row (the lowest index among
+// equal maxima; NaN never wins). One workgroup per row.
+__global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ x, int V, int32_t* __restrict__ out) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const float* row = x + (int64_t)blockIdx.x * V;
+  float best = -INFINITY;
+  int bi = 0x7FFFFFFF;
+  for (int i = threadIdx.x; i < V; i += 256) {
+    const float v = row[i];
+    if (v > best || (v == best && i < bi)) { best = v; bi = i; }
+  }
+  // wave: pairwise (value, index) maxima through lane swaps of distance 32..1
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) {
+    const float ov = __shfl_xor(best, d);
+    const int oi = __shfl_xor(bi, d);
+    if (ov > best || (ov == best && oi < bi)) { best = ov; bi = oi; }
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) { sv[w] = best; si[w] = bi; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < 4; ++k)
+      if (sv[k] > best || (sv[k] == best && si[k] < bi)) { best = sv[k]; bi = si[k]; }
+    out[blockIdx.x] = bi == 0x7FFFFFFF ? 0 : bi;  // a row of NaNs or -inf gives 0
+  }
+}
+
+void launch_argmax(hipStream_t s, const float* x, int n_rows, int V, int32_t* out) {
+  if (n_rows <= 0) return;
+  argmax_kernel<<<n_rows, 256, 0, s>>>(x, V, out);
+}
+
 }  // namespace hb

@@ -125,7 +125,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
         const int n = nb * BN + wn * 64 + 16 * ni + cq;
         if (n >= N) continue;
         f32x4 c = acc[mi][ni];
-        if (EPI == GEMM_RESIDUAL) {
+        if (EPI == GEMM_RESIDUAL && a.R) {
           if (a.r_f32) {
             const u32x4 r = ld16(reinterpret_cast<const float*>(a.R) + (size_t)m * a.ldr + n);
             for (int j = 0; j < 4; ++j) c[j] += __uint_as_float(r[j]);
@@ -517,7 +517,7 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
         const int n = nt * BN + wn * WN + 16 * ni + cq;
         if (n >= N) continue;
         f32x4 c = acc[mi][ni];
-        if (EPI == GEMM_RESIDUAL) {
+        if (EPI == GEMM_RESIDUAL && a.R) {
           if (a.r_f32) {
             const u32x4 rr = ld16(reinterpret_cast<const float*>(a.R) + (size_t)m * a.ldr + n);
             for (int j = 0; j < 4; ++j) c[j] += __uint_as_float(rr[j]);
@@ -628,7 +628,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, const fl
       st8(reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + n, o);
       continue;
     }
-    if (EPI == GEMM_RESIDUAL) {
+    if (EPI == GEMM_RESIDUAL && a.R) {
       if (a.r_f32) {
         const u32x4 rr = ld16(reinterpret_cast<const float*>(a.R) + (size_t)m * a.ldr + n);
         for (int j = 0; j < 4; ++j) c[j] += __uint_as_float(rr[j]);
@@ -667,7 +667,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_rmsnorm_kernel(GemmArgs a, 
       const float* p = partial + (size_t)row * N + 8 * vi;
       const f32x4 c0 = sum_splits<KS>(p, split_stride), c1 = sum_splits<KS>(p + 4, split_stride);
       float c[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
-      if (a.r_f32) {
+      if (!a.R) {
+      } else if (a.r_f32) {
         const float* rr = reinterpret_cast<const float*>(a.R) + (size_t)row * a.ldr + 8 * vi;
         const u32x4 r0 = ld16(rr), r1 = ld16(rr + 4);
         for (int j = 0; j < 4; ++j) { c[j] += __uint_as_float(r0[j]); c[4 + j] += __uint_as_float(r1[j]); }

@@ -100,3 +100,51 @@ class DeviceLayer:
         torch.cuda.synchronize()
         _hip_memcpy_d2d(out.data_ptr(), ptr, out.numel() * out.element_size())
         return out
+
+
+class DeviceModel:
+    """A whole model (hb_model): per-layer weights and paged pools, token
+    embedding, final gain and LM head on the current GPU."""
+
+    def __init__(self, shape, model_bits: Dict, num_blocks: int, max_batch_tokens: int, max_requests: int,
+                 pool_fill_bits: Optional[int] = 0, device: str = "cuda"):
+        torch = _torch()
+        self.shape = shape
+        self.device = device
+        self.num_blocks = int(num_blocks)
+        self.w = [{n: to_device_bf16(lw[n], device) for n in WEIGHT_NAMES} for lw in model_bits["layers"]]
+        nkv, hd = shape.n_kv_heads, shape.head_dim
+        self.pools = []
+        for _ in self.w:
+            k = torch.empty((num_blocks, nkv, 16, hd), dtype=torch.bfloat16, device=device)
+            v = torch.empty((num_blocks, nkv, 2, hd, 8), dtype=torch.bfloat16, device=device)
+            if pool_fill_bits is not None:
+                fill = int(np.array([pool_fill_bits], dtype=np.uint16).view(np.int16)[0])
+                k.view(torch.int16).fill_(fill)
+                v.view(torch.int16).fill_(fill)
+            self.pools.append((k, v))
+        self.embed = to_device_bf16(model_bits["embed"], device)
+        self.lm_head = to_device_bf16(model_bits["lm_head"], device)
+        self.g_final = to_device_bf16(model_bits["g_final"], device)
+        self.vocab = int(self.embed.shape[0])
+        self.cfg = hb.make_config(shape, max_batch_tokens, max_requests)
+        self.model = hb.hb_create_model(self.cfg, self.w, self.pools, num_blocks, self.embed, self.g_final,
+                                        self.lm_head)
+
+    def append_kv(self, layer: int, block_table, context_len: int, k_bits: np.ndarray, v_bits: np.ndarray) -> None:
+        if k_bits.shape[0] == 0:
+            return
+        k = to_device_bf16(k_bits, self.device)
+        v = to_device_bf16(v_bits, self.device)
+        hb.hb_append_kv(self.model.layer(layer), block_table, context_len, k, v)
+        _torch().cuda.current_stream().synchronize()  # k, v are freed on return
+
+    def run(self, requests: Sequence[Tuple[int, int, np.ndarray]], token_ids: np.ndarray, keep_logits: bool = True):
+        """Enqueue one model iteration; returns (next_tokens int32 [R], logits fp32 [R][vocab] or None)."""
+        torch = _torch()
+        ids = torch.from_numpy(np.ascontiguousarray(token_ids, dtype=np.int32)).to(self.device)
+        nxt = torch.empty(len(requests), dtype=torch.int32, device=self.device)
+        logits = torch.empty((len(requests), self.vocab), dtype=torch.float32, device=self.device) if keep_logits else None
+        hb.hb_run_model(self.model, requests, ids, nxt, logits)
+        self._ids = ids  # alive until the caller synchronises
+        return nxt, logits

@@ -21,6 +21,7 @@ HB_STAGE_Q, HB_STAGE_ATTN, HB_STAGE_H2, HB_STAGE_MLP = range(4)
 
 EXPORTED = ("hb_create_layer", "hb_destroy_layer", "hb_append_kv", "hb_run_iteration", "hb_validate_batch",
             "hb_profile", "hb_profile_batches", "hb_latency_features", "hb_fit_latency_model", "hb_predict_latency", "hb_select_chunk",
+            "hb_create_model", "hb_destroy_model", "hb_model_layer", "hb_run_model",
             "hb_set_kernel_timing", "hb_kernel_times", "hb_kernel_name", "hb_layer_stage", "hb_last_error")
 HB_LAT_FEATURES = 5
 
@@ -60,6 +61,17 @@ class hb_profile_cell(C.Structure):
 
 class hb_latency_model(C.Structure):
     _fields_ = [("coef", C.c_double * HB_LAT_FEATURES), ("fit_rel_rms", C.c_double), ("n_cells", C.c_int32)]
+
+
+class hb_model_desc(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("vocab", C.c_int32), ("layers", C.POINTER(hb_layer_weights)),
+                ("pools", C.POINTER(hb_kv_pool)), ("embed", C.c_void_p), ("g_final", C.c_void_p),
+                ("lm_head", C.c_void_p)]
+
+
+class hb_model_batch(C.Structure):
+    _fields_ = [("n_requests", C.c_int32), ("requests", C.POINTER(hb_request)), ("token_ids", C.c_void_p),
+                ("logits", C.c_void_p), ("next_tokens", C.c_void_p)]
 
 
 class HBError(RuntimeError):
@@ -115,6 +127,15 @@ def load() -> C.CDLL:
                                     C.POINTER(C.c_double), C.c_int32, C.c_double, C.c_int32, C.c_int32, C.c_int32,
                                     C.POINTER(C.c_int32), C.POINTER(C.c_double)]
     lib.hb_select_chunk.restype = st
+    lib.hb_create_model.argtypes = [C.POINTER(hb_layer_config), C.POINTER(hb_model_desc), C.c_void_p,
+                                    C.POINTER(C.c_void_p)]
+    lib.hb_create_model.restype = st
+    lib.hb_destroy_model.argtypes = [C.c_void_p]
+    lib.hb_destroy_model.restype = None
+    lib.hb_model_layer.argtypes = [C.c_void_p, C.c_int32]
+    lib.hb_model_layer.restype = C.c_void_p
+    lib.hb_run_model.argtypes = [C.c_void_p, C.POINTER(hb_model_batch)]
+    lib.hb_run_model.restype = st
     lib.hb_set_kernel_timing.argtypes = [C.c_void_p, C.c_uint32]
     lib.hb_set_kernel_timing.restype = st
     lib.hb_kernel_times.argtypes = [C.c_void_p, C.POINTER(C.c_double), C.POINTER(C.c_int64), C.c_int32]
@@ -146,7 +167,10 @@ def make_config(shape, max_batch_tokens: int, max_requests: int) -> hb_layer_con
 
 
 class Layer:
-    """Owns an hb_layer handle and keeps the tensors it points at alive."""
+    """Owns an hb_layer handle (unless borrowed from a model) and keeps the
+    tensors it points at alive."""
+
+    borrowed = False
 
     def __init__(self, handle: C.c_void_p, cfg: hb_layer_config, keep: list):
         self.handle = handle
@@ -155,9 +179,71 @@ class Layer:
 
     def __del__(self):
         try:
-            hb_destroy_layer(self)
+            if not self.borrowed:
+                hb_destroy_layer(self)
         except Exception:
             pass
+
+
+class Model:
+    """Owns an hb_model handle and keeps the tensors it points at alive."""
+
+    def __init__(self, handle: C.c_void_p, cfg: hb_layer_config, n_layers: int, vocab: int, keep: list):
+        self.handle = handle
+        self.cfg = cfg
+        self.n_layers = n_layers
+        self.vocab = vocab
+        self._keep = keep
+
+    def layer(self, index: int) -> "Layer":
+        """Borrowed handle of layer `index` (the model destroys it)."""
+        h = load().hb_model_layer(self.handle, int(index))
+        if not h:
+            raise IndexError(index)
+        lay = Layer(C.c_void_p(h), self.cfg, [self])
+        lay.borrowed = True
+        return lay
+
+    def __del__(self):
+        try:
+            hb_destroy_model(self)
+        except Exception:
+            pass
+
+
+def hb_create_model(cfg: hb_layer_config, layer_weights: Sequence[Dict[str, "torch.Tensor"]], pools,
+                    num_blocks: int, embed, g_final, lm_head, stream: Optional[int] = None) -> Model:
+    """pools: [(k_pool, v_pool)] per layer."""
+    n = len(layer_weights)
+    wa = (hb_layer_weights * n)()
+    pa = (hb_kv_pool * n)()
+    for i, (w, (kp, vp)) in enumerate(zip(layer_weights, pools)):
+        wa[i] = hb_layer_weights(*(_ptr(w[k]) for k in ("w_qkv", "w_o", "w_gate_up", "w_down", "g_attn", "g_ffn")))
+        pa[i] = hb_kv_pool(_ptr(kp), _ptr(vp), int(num_blocks))
+    vocab = int(embed.shape[0])
+    d = hb_model_desc(n, vocab, wa, pa, C.c_void_p(_ptr(embed)), C.c_void_p(_ptr(g_final)), C.c_void_p(_ptr(lm_head)))
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream().cuda_stream
+    h = C.c_void_p()
+    _check(load().hb_create_model(C.byref(cfg), C.byref(d), C.c_void_p(stream), C.byref(h)))
+    return Model(h, cfg, n, vocab, [layer_weights, pools, embed, g_final, lm_head])
+
+
+def hb_destroy_model(model: Model) -> None:
+    if model.handle is not None and model.handle.value:
+        load().hb_destroy_model(model.handle)
+        model.handle = None
+
+
+def hb_run_model(model: Model, requests: Sequence[Tuple[int, int, Iterable[int]]], token_ids, next_tokens,
+                 logits=None) -> None:
+    """token_ids: device int32 [T]; next_tokens: device int32 [n_requests];
+    logits: device fp32 [n_requests][vocab] or None."""
+    d, keep = _desc(requests, 0, 0, HB_OUT_BF16)
+    b = hb_model_batch(len(requests), d.requests, C.c_void_p(_ptr(token_ids)), C.c_void_p(_ptr(logits)),
+                       C.c_void_p(_ptr(next_tokens)))
+    _check(load().hb_run_model(model.handle, C.byref(b)))
 
 
 def _ptr(t) -> int:

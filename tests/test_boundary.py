@@ -116,3 +116,33 @@ def test_config_errors(H, field, value, status):
 def test_gqa_group_must_divide_16(H):
     shape = type("S", (Shape,), {"n_q_heads": 32, "n_kv_heads": 1})
     assert _v(H, [(1, 0, bt(1))], shape=shape) == H.HB_ERR_UNSUPPORTED
+
+
+def _create_model(H, n_layers=2, vocab=64, pool_blocks=(64, 64), null_embed=False):
+    """hb_create_model with fake device addresses: every case here must be
+    rejected before any HIP call."""
+    import ctypes as C
+    cfg = H.make_config(Shape, 128, 8)
+    n = max(n_layers, 1)
+    wa = (H.hb_layer_weights * n)()
+    pa = (H.hb_kv_pool * n)()
+    for i in range(n):
+        wa[i] = H.hb_layer_weights(*[0x1000 * (j + 1) for j in range(6)])
+        pa[i] = H.hb_kv_pool(0x30000000, 0x40000000, pool_blocks[i % len(pool_blocks)])
+    d = H.hb_model_desc(n_layers, vocab, wa, pa, C.c_void_p(0 if null_embed else 0x50000000),
+                        C.c_void_p(0x60000000), C.c_void_p(0x70000000))
+    h = C.c_void_p()
+    st = H.load().hb_create_model(C.byref(cfg), C.byref(d), None, C.byref(h))
+    assert not h.value
+    return st
+
+
+@pytest.mark.parametrize("kw", [dict(n_layers=0), dict(vocab=60), dict(vocab=0), dict(pool_blocks=(64, 32)),
+                                dict(null_embed=True)], ids=str)
+def test_model_argument_errors(H, kw):
+    assert _create_model(H, **kw) == H.HB_ERR_INVALID
+    assert H.hb_last_error()
+
+
+def test_model_layer_of_null_model(H):
+    assert not H.load().hb_model_layer(None, 0)

@@ -372,3 +372,42 @@ def test_tiny_workload_runs_through_oracle():
     oracle.seed_cache(cache, b.requests, lambda r: tuple(oracle.bf16_bits_to_f64(a) for a in b.prior_kv(r)))
     y = oracle.layer_forward(w, TINY, cache, b.requests, oracle.bf16_bits_to_f64(b.x_in()))
     assert y.shape == (72, 256) and np.all(np.isfinite(y))
+
+
+def test_round_bf16_matches_torch_and_ties_to_even():
+    """The model oracle's inter-layer rounding equals torch's bfloat16
+    conversion (a library routine, RNE) on random and edge values."""
+    import torch
+    from oracle.model import round_bf16
+    rng = np.random.default_rng(7)
+    x = np.concatenate([rng.standard_normal(10000) * 10 ** rng.uniform(-6, 6, 10000),
+                        [0.0, -0.0, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, 65504.0, 1e-40]])
+    want = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(round_bf16(x), want)
+
+
+def test_model_chunk_split_equals_unsplit():
+    """Whole-model invariant: a prompt processed in one chunk or in two gives
+    the same last-token logits (every layer's cache holds the first chunk's
+    K/V when the second runs)."""
+    from hb_workloads import make_batch, make_model_weights
+    from oracle.model import model_forward
+    shape = TINY
+    mw = make_model_weights(shape, 2, 64)
+    lw = [oracle.weights_to_f64(w) for w in mw["layers"]]
+    emb, head = oracle.bf16_bits_to_f64(mw["embed"]), oracle.bf16_bits_to_f64(mw["lm_head"])
+    g = oracle.bf16_bits_to_f64(mw["g_final"])
+    b = make_batch(shape, [(48, 0)], seed=5, num_blocks=64)
+    ids = b.token_ids(64)
+    req = b.requests[0]
+
+    def caches():
+        return [oracle.PagedKVCache(64, shape.n_kv_heads, shape.head_dim) for _ in lw]
+
+    whole, _ = model_forward(shape, lw, caches(), emb, g, head, b.requests, ids)
+    cs = caches()
+    first = [type(req)(30, 0, req.block_table)]
+    second = [type(req)(18, 30, req.block_table)]
+    model_forward(shape, lw, cs, emb, g, head, first, ids[:30])
+    split, _ = model_forward(shape, lw, cs, emb, g, head, second, ids[30:])
+    assert np.allclose(whole, split, rtol=0, atol=1e-9)
