@@ -229,6 +229,110 @@ def fit_and_validate_latency_model(hb, dl, shape, mixes, median_ms, iters):
             "timing": "kernel time per iteration, 512 MiB write before each (hb_profile / hb_profile_batches)"}
 
 
+class DeviceRandomLayer:
+    """A layer whose weights and paged pool are drawn on the device from a
+    seed (for timing only: values need realistic scale, not the oracle's
+    exact draws); exposes .layer and .run like the harness's DeviceLayer."""
+
+    def __init__(self, hb, torch, shape, num_blocks, max_T, max_R, seed):
+        self.hb, self.torch = hb, torch
+        g = torch.Generator(device="cuda")
+        g.manual_seed(seed)
+        self.w = random_layer_weights(torch, shape, g)
+        nkv, hd = shape.n_kv_heads, shape.head_dim
+        self.k = torch.randn((num_blocks, nkv, 16, hd), generator=g, device="cuda", dtype=torch.bfloat16)
+        self.v = torch.randn((num_blocks, nkv, 2, hd, 8), generator=g, device="cuda", dtype=torch.bfloat16)
+        self.layer = hb.hb_create_layer(hb.make_config(shape, max_T, max_R), self.w, self.k, self.v, num_blocks)
+
+    def run(self, reqs, x, out_dtype, y):
+        self.hb.hb_run_iteration(self.layer, reqs, x, y, out_dtype)
+        return y
+
+
+def random_layer_weights(torch, shape, g):
+    H, F, nq, nkv, hd = shape.hidden, shape.ffn_dim, shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+
+    def randn(rows, cols, std):
+        return (torch.randn((rows, cols), generator=g, device="cuda") * std).to(torch.bfloat16)
+
+    return {"w_qkv": randn((nq + 2 * nkv) * hd, H, H ** -0.5), "w_o": randn(H, nq * hd, (nq * hd) ** -0.5),
+            "w_gate_up": randn(2 * F, H, H ** -0.5), "w_down": randn(H, F, F ** -0.5),
+            "g_attn": (1 + 0.1 * torch.randn(H, generator=g, device="cuda")).to(torch.bfloat16),
+            "g_ffn": (1 + 0.1 * torch.randn(H, generator=g, device="cuda")).to(torch.bfloat16)}
+
+
+def blas_ceiling(torch, shape, M, steps=10):
+    """Context only: torch.matmul (hipBLASLt) on the layer's four GEMM shapes
+    at M rows, no epilogues (microseconds, TFLOP/s)."""
+    H, F, qd, qkv_n = shape.hidden, shape.ffn_dim, shape.n_q_heads * shape.head_dim, \
+        (shape.n_q_heads + 2 * shape.n_kv_heads) * shape.head_dim
+    out = {}
+    for name, N, K in (("gemm_qkv", qkv_n, H), ("gemm_o", H, qd), ("gemm_gate_up", 2 * F, H), ("gemm_down", H, F)):
+        a = torch.randn((M, K), device="cuda").to(torch.bfloat16)
+        w = torch.randn((N, K), device="cuda").to(torch.bfloat16)
+        for _ in range(3):
+            c = a @ w.t()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            c = a @ w.t()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / steps * 1e3
+        out[name] = {"us": round(us, 1), "tflops": round(2.0 * M * N * K / us / 1e6, 1)}
+        del a, w, c
+    tot_us = sum(v["us"] for v in out.values())
+    tot_fl = sum(2.0 * M * N * K for N, K in ((qkv_n, H), (H, qd), (2 * F, H), (H, F)))
+    out["four_gemms"] = {"us": round(tot_us, 1), "mfma_frac": round(tot_fl / (tot_us * 1e-6) / PEAK_BF16, 4)}
+    return out
+
+
+def gate_cells(hb, torch, dl, shape, steps, with_70b=True):
+    """The fixed gate sets of the layer's targets: attention's HBM fraction on
+    decode-heavy sweep cells (chunk 128/256 x 128/256 decodes), the four
+    GEMMs' MFMA fraction on chunk-heavy cells (chunk 1024/2048 x 0/32 decodes)
+    and on the 70B layer (chunk 2048 at 30720 + 32 decodes at 32768); with
+    hipBLASLt on the same GEMM shapes as context."""
+    from hb_workloads import LLAMA3_70B, llama70b_batch, sweep_batch
+    from paper_2503_22562_amd.harness import to_device_bf16
+
+    def cell(layer, b, shp):
+        x = to_device_bf16(b.x_in())
+        y = torch.empty((b.n_tokens, shp.hidden), dtype=torch.float32, device="cuda")
+        kt = regime(hb, layer, b, shp, x, y, steps)
+        at_s, at_f, at_b = kt["attention"]
+        gem = {k: v for k, v in kt.items() if k.startswith("gemm_")}
+        g_s = sum(t for t, _, _ in gem.values())
+        g_f = sum(f for _, f, _ in gem.values())
+        return {"layer_ms": round(sum(t for t, _, _ in kt.values()) * 1e3, 4),
+                "attention_ms": round(at_s * 1e3, 4), "attention_hbm_frac": round(at_b / at_s / PEAK_HBM, 4),
+                "attention_mfma_frac": round(at_f / at_s / PEAK_BF16, 4),
+                "gemms_ms": round(g_s * 1e3, 4), "gemms_mfma_frac": round(g_f / g_s / PEAK_BF16, 4),
+                "per_gemm_tflops": {k: round(f / t / 1e12, 1) for k, (t, f, _) in sorted(gem.items())}}
+
+    out = {"decode_heavy": {}, "chunk_heavy": {}}
+    for c in (128, 256):
+        for n in (128, 256):
+            out["decode_heavy"][f"chunk {c} + {n} decodes"] = cell(dl, sweep_batch(c, n), shape)
+    for c in (1024, 2048):
+        for n in (0, 32):
+            out["chunk_heavy"][f"chunk {c} + {n} decodes"] = cell(dl, sweep_batch(c, n), shape)
+    out["blas_ceiling_8b_m2048"] = blas_ceiling(torch, shape, 2048)
+    if with_70b:
+        b70 = llama70b_batch()
+        l70 = DeviceRandomLayer(hb, torch, LLAMA3_70B, b70.num_blocks, b70.n_tokens, 64, 170)
+        out["chunk_heavy"]["llama3-70b: chunk 2048 at 30720 + 32 decodes at 32768"] = cell(l70, b70, LLAMA3_70B)
+        del l70
+        torch.cuda.empty_cache()
+        out["blas_ceiling_70b_m2080"] = blas_ceiling(torch, LLAMA3_70B, 2080)
+    dh = [v["attention_hbm_frac"] for v in out["decode_heavy"].values()]
+    ch = [v["gemms_mfma_frac"] for v in out["chunk_heavy"].values()]
+    out["summary"] = {"decode_heavy_attention_hbm_frac_min": min(dh), "target_hbm": 0.60,
+                      "chunk_heavy_gemms_mfma_frac_min": min(ch), "chunk_heavy_gemms_mfma_frac_max": max(ch),
+                      "target_mfma": 0.50}
+    return out
+
+
 def model_iteration(hb, torch, shape, batch_lens, seed, n_layers=32, vocab=128256, steps=20, warmup=3):
     """Whole-model iteration (hb_run_model): n_layers decoder layers of the
     given shape between a token embedding and the LM head, on the same
@@ -243,19 +347,13 @@ def model_iteration(hb, torch, shape, batch_lens, seed, n_layers=32, vocab=12825
     g.manual_seed(seed)
     H, F, nq, nkv, hd = shape.hidden, shape.ffn_dim, shape.n_q_heads, shape.n_kv_heads, shape.head_dim
 
-    def randn(rows, cols, std):
-        return (torch.randn((rows, cols), generator=g, device="cuda") * std).to(torch.bfloat16)
-
     layers, pools = [], []
     for _ in range(n_layers):
-        layers.append({"w_qkv": randn((nq + 2 * nkv) * hd, H, H ** -0.5), "w_o": randn(H, nq * hd, (nq * hd) ** -0.5),
-                       "w_gate_up": randn(2 * F, H, H ** -0.5), "w_down": randn(H, F, F ** -0.5),
-                       "g_attn": (1 + 0.1 * torch.randn(H, generator=g, device="cuda")).to(torch.bfloat16),
-                       "g_ffn": (1 + 0.1 * torch.randn(H, generator=g, device="cuda")).to(torch.bfloat16)})
+        layers.append(random_layer_weights(torch, shape, g))
         pools.append((torch.randn((nb, nkv, 16, hd), generator=g, device="cuda", dtype=torch.bfloat16),
                       torch.randn((nb, nkv, 2, hd, 8), generator=g, device="cuda", dtype=torch.bfloat16)))
     embed = torch.randn((vocab, H), generator=g, device="cuda", dtype=torch.bfloat16)
-    head = randn(vocab, H, H ** -0.5)
+    head = (torch.randn((vocab, H), generator=g, device="cuda") * H ** -0.5).to(torch.bfloat16)
     g_final = (1 + 0.1 * torch.randn(H, generator=g, device="cuda")).to(torch.bfloat16)
     cfg = hb.make_config(shape, max(b.n_tokens, 1), max(len(b.requests), 1))
     model = hb.hb_create_model(cfg, layers, pools, nb, embed, g_final, head)
@@ -409,35 +507,12 @@ def main() -> int:
     flops, bytes_ = layer_work(shape, [(c, xx) for c, xx, _ in reqs])
     step_s = ms_per_step * 1e-3
 
-    # the two regimes the layer's targets name: attention's HBM rate on a
-    # decode-heavy batch, the GEMMs' MFMA rate on a chunk-heavy one
-    from hb_workloads import sweep_batch
-    regimes = None if a.no_regimes else {}
-    if regimes is not None:
-        dec = sweep_batch(128, 256)
-        xd = to_device_bf16(dec.x_in())
-        yd = torch.empty((dec.n_tokens, shape.hidden), dtype=torch.float32, device="cuda")
-        kt = regime(hb, dl, dec, shape, xd, yd, a.regime_steps)
-        at_s, _, at_b = kt["attention"]
-        regimes["decode_heavy"] = {
-            "cell": "chunk 128 + 256 decodes, contexts log-uniform 256..8192",
-            "kernel": "attention", "avg_ms": round(at_s * 1e3, 5), "gbps": round(at_b / at_s / 1e9, 1),
-            "hbm_frac": round(at_b / at_s / PEAK_HBM, 4),
-            "layer_ms": round(sum(t for t, _, _ in kt.values()) * 1e3, 4)}
-        chk = sweep_batch(2048, 0)
-        xc = to_device_bf16(chk.x_in())
-        yc = torch.empty((chk.n_tokens, shape.hidden), dtype=torch.float32, device="cuda")
-        kt = regime(hb, dl, chk, shape, xc, yc, a.regime_steps)
-        gem = {k: v for k, v in kt.items() if k.startswith("gemm_")}
-        g_s = sum(t for t, _, _ in gem.values())
-        g_f = sum(f for _, f, _ in gem.values())
-        regimes["chunk_heavy"] = {
-            "cell": "chunk 2048 + 0 decodes", "kernels": "the four GEMMs (split-K reduces included)",
-            "avg_ms": round(g_s * 1e3, 5), "tflops": round(g_f / g_s / 1e12, 1),
-            "mfma_frac": round(g_f / g_s / PEAK_BF16, 4),
-            "per_gemm_tflops": {k: round(f / t / 1e12, 1) for k, (t, f, _) in sorted(gem.items())},
-            "layer_ms": round(sum(t for t, _, _ in kt.values()) * 1e3, 4)}
-        del xd, yd, xc, yc
+    # the gate cells of the layer's targets (decode-heavy: attention's HBM
+    # rate; chunk-heavy: the GEMMs' MFMA rate), hipBLASLt as context
+    gates = None
+    if not a.no_regimes:
+        log("bench: gate cells (decode-heavy and chunk-heavy sweep cells, 70B layer, hipBLASLt ceiling)")
+        gates = gate_cells(hb, torch, dl, shape, a.regime_steps)
 
     profile = None
     if not a.no_profile:
@@ -502,8 +577,10 @@ def main() -> int:
         "kernels": kernels,
         "kernels_note": "per-kernel averages from a separate pass with every launch bracketed by events",
         "cpu_baseline": cpu,
-        "regimes": regimes,
-        "regimes_note": "per-kernel averages with every launch bracketed by events; algorithmic work as for roofline",
+        "gates": gates,
+        "gates_note": "per-kernel averages with every launch bracketed by events; algorithmic work as for roofline; "
+                      "GEMM times include their split-K reduces; blas_ceiling = torch.matmul on the same shapes "
+                      "without epilogues (context, not a target)",
         "latency_profile": profile,
         "latency_model": latency_model,
         "model_iteration": model,
