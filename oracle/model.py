@@ -38,13 +38,17 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
 
 
 def model_forward(cfg, layer_weights: Sequence[dict], caches, embed: np.ndarray, g_final: np.ndarray,
-                  lm_head: np.ndarray, requests, token_ids: np.ndarray):
+                  lm_head: np.ndarray, requests, token_ids: np.ndarray, round_between: bool = True):
     """Returns (logits [n_requests][vocab] of each request's last row, next
     token ids). layer_weights / caches: fp64 weights and a PagedKVCache per
-    layer (prior contexts already stored); embed, lm_head: fp64 [vocab][H]."""
+    layer (prior contexts already stored); embed, lm_head: fp64 [vocab][H].
+    round_between=False keeps the hidden states in fp64 between layers (the
+    plain definition of the stack, used to pin it)."""
     x = embed[np.asarray(token_ids, dtype=np.int64)]
     for w, cache in zip(layer_weights, caches):
-        x = round_bf16(layer_forward(w, cfg, cache, requests, x))
+        x = layer_forward(w, cfg, cache, requests, x)
+        if round_between:
+            x = round_bf16(x)
     last = np.cumsum([int(r.chunk_len) for r in requests]) - 1
     h = rmsnorm(x[last], g_final, cfg.rms_eps)
     logits = h @ lm_head.T

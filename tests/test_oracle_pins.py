@@ -411,3 +411,59 @@ def test_model_chunk_split_equals_unsplit():
     model_forward(shape, lw, cs, emb, g, head, first, ids[:30])
     split, _ = model_forward(shape, lw, cs, emb, g, head, second, ids[30:])
     assert np.allclose(whole, split, rtol=0, atol=1e-9)
+
+
+def test_model_matches_textbook_causal_lm():
+    """The model oracle with fp64 hidden states between layers equals HF
+    transformers' LlamaForCausalLM (fp64, eager, untied head) on the last
+    token's logits: one prompt as a single chunk, and the same prompt as two
+    iterations (a chunk, then the rest beside a decode of another request)."""
+    from transformers import LlamaConfig, LlamaForCausalLM
+    from oracle.model import model_forward
+    cfg = Cfg(hidden=64, nq=4, nkv=2, hd=16, ffn=96)
+    vocab, n_layers = 48, 2
+    rng = np.random.default_rng(1234)
+    lw = [rand_weights(cfg, rng) for _ in range(n_layers)]
+    embed = rng.standard_normal((vocab, cfg.hidden))
+    head = rng.standard_normal((vocab, cfg.hidden)) / np.sqrt(cfg.hidden)
+    g_final = 1.0 + 0.1 * rng.standard_normal(cfg.hidden)
+    hc = LlamaConfig(vocab_size=vocab, hidden_size=cfg.hidden, num_hidden_layers=n_layers,
+                     num_attention_heads=cfg.n_q_heads, num_key_value_heads=cfg.n_kv_heads, head_dim=cfg.head_dim,
+                     intermediate_size=cfg.ffn_dim, rms_norm_eps=cfg.rms_eps, rope_theta=cfg.rope_theta,
+                     attention_bias=False, mlp_bias=False, tie_word_embeddings=False, max_position_embeddings=256)
+    hc._attn_implementation = "eager"
+    m = LlamaForCausalLM(hc).double().eval()
+    nq, nkv, hd, f = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.ffn_dim
+    sd = {"model.embed_tokens.weight": embed, "model.norm.weight": g_final, "lm_head.weight": head}
+    for i, w in enumerate(lw):
+        p = f"model.layers.{i}."
+        sd.update({p + "self_attn.q_proj.weight": w["w_qkv"][: nq * hd],
+                   p + "self_attn.k_proj.weight": w["w_qkv"][nq * hd:(nq + nkv) * hd],
+                   p + "self_attn.v_proj.weight": w["w_qkv"][(nq + nkv) * hd:],
+                   p + "self_attn.o_proj.weight": w["w_o"], p + "mlp.gate_proj.weight": w["w_gate_up"][:f],
+                   p + "mlp.up_proj.weight": w["w_gate_up"][f:], p + "mlp.down_proj.weight": w["w_down"],
+                   p + "input_layernorm.weight": w["g_attn"], p + "post_attention_layernorm.weight": w["g_ffn"]})
+    missing, unexpected = m.load_state_dict({k: torch.from_numpy(np.ascontiguousarray(v)) for k, v in sd.items()},
+                                            strict=False)
+    assert not unexpected and all("rotary" in k for k in missing)
+    # fp64 RoPE frequencies (the library still forms the angles p * freq in
+    # fp32, an error of ~1e-7 in the logits, hence the tolerance below)
+    m.model.rotary_emb.inv_freq = torch.from_numpy(cfg.rope_theta ** (-np.arange(0, hd, 2, dtype=np.float64) / hd))
+    ids = rng.integers(0, vocab, 37)
+    with torch.no_grad():
+        ref = m(torch.from_numpy(ids)[None]).logits[0, -1].numpy()
+
+    def caches():
+        return [oracle.PagedKVCache(32, nkv, hd) for _ in lw]
+
+    bt = [5, 17, 2]
+    got, nxt = model_forward(cfg, lw, caches(), embed, g_final, head, [Req(37, 0, bt)], ids, round_between=False)
+    np.testing.assert_allclose(got[0], ref, rtol=1e-5, atol=1e-6)
+    assert nxt[0] == int(np.argmax(ref))
+    cs = caches()
+    other = [9]
+    model_forward(cfg, lw, cs, embed, g_final, head, [Req(20, 0, bt), Req(1, 0, other)],
+                  np.concatenate([ids[:20], [3]]), round_between=False)
+    got2, _ = model_forward(cfg, lw, cs, embed, g_final, head, [Req(1, 1, other), Req(17, 20, bt)],
+                            np.concatenate([[4], ids[20:]]), round_between=False)
+    np.testing.assert_allclose(got2[1], ref, rtol=1e-5, atol=1e-6)
