@@ -150,3 +150,25 @@ def test_model_rejects_bad_batches(hb):
     with pytest.raises(H.HBError) as e:
         dm.run(bad, ids[:1])
     assert e.value.status == H.HB_ERR_RANGE
+
+
+def test_llama8b_shaped_two_layer_model_full_vocab(hb):
+    """Two Llama-3-8B-shaped layers and a 128256-row LM head on a hybrid batch
+    (a 96-token chunk at context 200 plus 16 decodes): every request's logits
+    against the fp64 oracle, at the model bar for two layers."""
+    import torch
+    from hb_workloads import LLAMA3_8B
+    vocab = 128256
+    mw = make_model_weights(LLAMA3_8B, 2, vocab)
+    rng = np.random.default_rng(11)
+    lens = [(96, 200)] + [(1, int(c)) for c in rng.integers(1, 600, 16)]
+    b = make_batch(LLAMA3_8B, lens, seed=21, num_blocks=2048)
+    ids = b.token_ids(vocab)
+    dm = _device_model(b, mw, b.n_tokens, len(b.requests))
+    nxt, logits = dm.run(_reqs(b), ids)
+    torch.cuda.synchronize()
+    got = logits.cpu().numpy().astype(np.float64)
+    ref, _ = model_forward(LLAMA3_8B, *_oracle_model(b, mw), b.requests, ids)
+    print("8B-shaped 2-layer model logits", errors(got, ref))
+    ma = assert_model_parity(got, ref, 2)
+    _check_choice(nxt.cpu().numpy(), logits.cpu().numpy(), ref, ma)
