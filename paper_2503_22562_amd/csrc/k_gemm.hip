@@ -334,6 +334,41 @@ __device__ __forceinline__ void qkv_rope_row(const GemmArgs& a, const f32x4 (&ac
   }
 }
 
+// One accumulator row of a plain or residual epilogue: 4 columns per
+// fragment, TN fragments 16 columns apart from column nbase. RK: residual
+// none (0), bf16 (1) or fp32 (2); CF: fp32 (else bf16) output. All residual
+// loads are issued before the first add.
+template <int TN, int RK, bool CF>
+__device__ __forceinline__ void residual_row(const GemmArgs& a, const f32x4 (&acc)[TN], int m, int nbase) {
+  f32x4 r[TN];
+#pragma unroll
+  for (int ni = 0; ni < TN; ++ni) {
+    const int n = min(nbase + 16 * ni, a.N - 4);
+    if (RK == 2) {
+      const u32x4 rr = ld16(reinterpret_cast<const float*>(a.R) + (size_t)m * a.ldr + n);
+      r[ni] = f32x4{__uint_as_float(rr[0]), __uint_as_float(rr[1]), __uint_as_float(rr[2]), __uint_as_float(rr[3])};
+    } else if (RK == 1) {
+      const u32x2 rr = ld8(reinterpret_cast<const uint16_t*>(a.R) + (size_t)m * a.ldr + n);
+      r[ni] = f32x4{bf16_lo(rr[0]), bf16_hi(rr[0]), bf16_lo(rr[1]), bf16_hi(rr[1])};
+    } else {
+      r[ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+#pragma unroll
+  for (int ni = 0; ni < TN; ++ni) {
+    const int n = nbase + 16 * ni;
+    if (n >= a.N) continue;
+    const f32x4 c = acc[ni] + r[ni];
+    if (CF) {
+      const u32x4 o = {__float_as_uint(c[0]), __float_as_uint(c[1]), __float_as_uint(c[2]), __float_as_uint(c[3])};
+      st16(reinterpret_cast<float*>(a.C) + (size_t)m * a.ldc + n, o);
+    } else {
+      const u32x2 o = {pack_bf16x2(c[0], c[1]), pack_bf16x2(c[2], c[3])};
+      st8(reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + n, o);
+    }
+  }
+}
+
 template <int TM, int TN, int WR, int WC, int S, int EPI>
 __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int tiles_m, int tiles_n, int ksplit,
                                                                   int kchunk, float* __restrict__ partial) {
@@ -466,12 +501,16 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
   // the loads issued past the end land in LDS before the workgroup ends
   wait_vmcnt<0>();
 
-  // epilogue: acc[mi][ni][i] = C[m][n + i]
+  // epilogue: acc[mi][ni][i] = C[m][n + i]. Fragment rows go in groups of
+  // EPB, whose loads (residual, or cos/sin and pool slots) are in flight
+  // together: one memory round trip per group, about 16 TN registers per
+  // group. The K loop's fragment registers cover that in 4-wave tiles; the
+  // 8-wave tiles (two waves per SIMD) would spill, and take one row at a time.
+  constexpr int EPB = (NW == 4 && 16 / TN > 1) ? 16 / TN : 1;
   const int cq = fg << 2;
 #pragma unroll
   for (int mi = 0; mi < TM; ++mi) {
-    // keep the residual loads of one fragment row at a time in flight
-    __builtin_amdgcn_sched_barrier(0);
+    if (mi % EPB == 0) __builtin_amdgcn_sched_barrier(0);
     const int m = m0 + wm * WM + 16 * mi + fr;
     if (m >= M) continue;
     if (ksplit > 1) {
@@ -511,30 +550,22 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
         o[1] = pack_bf16x2(silu_f(gt[2]) * up[2], silu_f(gt[3]) * up[3]);
         st8(reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + n, o);
       }
-    } else {
-#pragma unroll
-      for (int ni = 0; ni < TN; ++ni) {
-        const int n = nt * BN + wn * WN + 16 * ni + cq;
-        if (n >= N) continue;
-        f32x4 c = acc[mi][ni];
-        if (EPI == GEMM_RESIDUAL && a.R) {
-          if (a.r_f32) {
-            const u32x4 rr = ld16(reinterpret_cast<const float*>(a.R) + (size_t)m * a.ldr + n);
-            for (int j = 0; j < 4; ++j) c[j] += __uint_as_float(rr[j]);
-          } else {
-            const u32x2 rr = ld8(reinterpret_cast<const uint16_t*>(a.R) + (size_t)m * a.ldr + n);
-            c[0] += bf16_lo(rr[0]); c[1] += bf16_hi(rr[0]);
-            c[2] += bf16_lo(rr[1]); c[3] += bf16_hi(rr[1]);
-          }
-        }
-        if (EPI == GEMM_RESIDUAL && a.c_f32) {
-          u32x4 o = {__float_as_uint(c[0]), __float_as_uint(c[1]), __float_as_uint(c[2]), __float_as_uint(c[3])};
-          st16(reinterpret_cast<float*>(a.C) + (size_t)m * a.ldc + n, o);
-        } else {
-          u32x2 o = {pack_bf16x2(c[0], c[1]), pack_bf16x2(c[2], c[3])};
-          st8(reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + n, o);
-        }
+    } else if (EPI == GEMM_RESIDUAL) {
+      // one straight-line row per residual / output kind (the kinds are
+      // uniform over the launch)
+      const int nb = nt * BN + wn * WN + cq;
+      if (!a.R) {
+        if (a.c_f32) residual_row<TN, 0, true>(a, acc[mi], m, nb);
+        else residual_row<TN, 0, false>(a, acc[mi], m, nb);
+      } else if (a.r_f32) {
+        if (a.c_f32) residual_row<TN, 2, true>(a, acc[mi], m, nb);
+        else residual_row<TN, 2, false>(a, acc[mi], m, nb);
+      } else {
+        if (a.c_f32) residual_row<TN, 1, true>(a, acc[mi], m, nb);
+        else residual_row<TN, 1, false>(a, acc[mi], m, nb);
       }
+    } else {
+      residual_row<TN, 0, false>(a, acc[mi], m, nt * BN + wn * WN + cq);
     }
   }
 }
