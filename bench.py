@@ -7,7 +7,7 @@ Prints one JSON line: new tokens/s, per-step latency, the roofline of the
 dominant kernel, the CPU oracle's rate on the same batch and the latency
 profile against chunk size that dynamic chunking consumes.
 
-    python bench.py [--gpus 1] [--steps 50] [--warmup 10]
+    python bench.py [--gpus 1] [--steps 200] [--warmup 20]
 """
 from __future__ import annotations
 
@@ -384,6 +384,13 @@ def model_iteration(hb, torch, shape, batch_lens, seed, n_layers=32, vocab=12825
                     "compare with the strictest QoS tier's 50 ms"}
 
 
+def device_info(torch):
+    p = torch.cuda.get_device_properties(0)
+    return {"name": p.name, "arch": getattr(p, "gcnArchName", None), "compute_units": p.multi_processor_count,
+            "hbm_gib": round(p.total_memory / 2 ** 30, 1),
+            "host_cores": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -391,7 +398,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
-    ap.add_argument("--profile-iters", type=int, default=15)
+    ap.add_argument("--profile-iters", type=int, default=100)
+    ap.add_argument("--profile-warmup", type=int, default=10)
     ap.add_argument("--regime-steps", type=int, default=10)
     ap.add_argument("--no-regimes", action="store_true")
     ap.add_argument("--no-model", action="store_true", help="skip the 32-layer whole-model iteration")
@@ -518,7 +526,7 @@ def main() -> int:
     if not a.no_profile:
         log("bench: latency profile (chunk x decode grid)")
         mixes = [(sweep_decode_contexts(n), 0) for n in SWEEP_DECODES]
-        prof = hb.hb_profile(dl.layer, SWEEP_CHUNKS, mixes, warmup=3, iters=a.profile_iters, seed=1)
+        prof = hb.hb_profile(dl.layer, SWEEP_CHUNKS, mixes, warmup=a.profile_warmup, iters=a.profile_iters, seed=1)
         med = prof["median_ms"]
         mono = all(med[i, j] * (1.01 if (n == 0 and SWEEP_CHUNKS[j] <= 256) else 1.0) >= med[i, j - 1]
                    for i, n in enumerate(SWEEP_DECODES) for j in range(1, len(SWEEP_CHUNKS)))
@@ -527,7 +535,8 @@ def main() -> int:
                    "tokens_per_s": np.round(prof["tokens_per_s"]).tolist(),
                    "hbm_frac": np.round(prof["hbm_frac"], 3).tolist(),
                    "mfma_frac": np.round(prof["mfma_frac"], 3).tolist(),
-                   "monotone_in_chunk": bool(mono), "cache": "512 MiB flush before each timed iteration"}
+                   "monotone_in_chunk": bool(mono), "cache": "512 MiB flush before each timed iteration",
+                   "iterations_per_cell": {"warmup": a.profile_warmup, "timed": a.profile_iters}}
 
     latency_model = None
     if not a.no_profile:
@@ -584,6 +593,7 @@ def main() -> int:
         "latency_profile": profile,
         "latency_model": latency_model,
         "model_iteration": model,
+        "device": device_info(torch),
     }
     print(json.dumps(out), flush=True)
     return 0
