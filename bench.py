@@ -152,6 +152,31 @@ def copy_calibration(nbytes=1 << 30, reps=3):
     return 0
 
 
+def counters_cell(cell, steps, warmup):
+    """Only the layer iterations of one gate cell, for counter passes
+    (rocprofv3 --pmc): 'C,D' = the 8B sweep cell with a C-token chunk and D
+    decodes, '70b' = the 70B layer's chunk 2048 at 30720 + 32 decodes."""
+    import torch
+    from hb_workloads import LLAMA3_8B, LLAMA3_70B, llama70b_batch, sweep_batch
+    from paper_2503_22562_amd import hb
+    from paper_2503_22562_amd.harness import to_device_bf16
+    torch.cuda.set_device(0)
+    if cell == "70b":
+        shape, b = LLAMA3_70B, llama70b_batch()
+    else:
+        c, d = (int(v) for v in cell.split(","))
+        shape, b = LLAMA3_8B, sweep_batch(c, d)
+    layer = DeviceRandomLayer(hb, torch, shape, b.num_blocks, b.n_tokens, max(len(b.requests), 1), 7)
+    reqs = [(q.chunk_len, q.context_len, q.block_table) for q in b.requests]
+    x = to_device_bf16(b.x_in())
+    y = torch.empty((b.n_tokens, shape.hidden), dtype=torch.float32, device="cuda")
+    for _ in range(warmup + steps):
+        layer.run(reqs, x, hb.HB_OUT_F32, y)
+    torch.cuda.synchronize()
+    print(json.dumps({"counters_cell": cell, "tokens": b.n_tokens, "iterations": warmup + steps}), flush=True)
+    return 0
+
+
 def regime(hb, dl, batch, shape, x_dev, y_dev, steps):
     """Per-kernel timing of one sweep cell: every launch bracketed by HIP
     events, the cell run `steps` times after two warm-up iterations."""
@@ -403,6 +428,8 @@ def main() -> int:
     ap.add_argument("--regime-steps", type=int, default=10)
     ap.add_argument("--no-regimes", action="store_true")
     ap.add_argument("--no-model", action="store_true", help="skip the 32-layer whole-model iteration")
+    ap.add_argument("--counters-cell", default=None,
+                    help="only run one gate cell ('C,D' or '70b') --warmup + --steps times (counter passes) and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration) and exit")
     a = ap.parse_args()
@@ -412,6 +439,8 @@ def main() -> int:
         return 2
     if a.copy_calibration:
         return copy_calibration()
+    if a.counters_cell:
+        return counters_cell(a.counters_cell, a.steps, a.warmup)
 
     import torch
     from hb_workloads import LLAMA3_8B, POOL_TOKENS, SWEEP_CHUNKS, SWEEP_DECODES, llama8b_batch, make_weights, \
