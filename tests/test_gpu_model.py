@@ -172,3 +172,23 @@ def test_llama8b_shaped_two_layer_model_full_vocab(hb):
     print("8B-shaped 2-layer model logits", errors(got, ref))
     ma = assert_model_parity(got, ref, 2)
     _check_choice(nxt.cpu().numpy(), logits.cpu().numpy(), ref, ma)
+
+
+def test_model_token_ids_out_of_range_read_nearest_row(hb):
+    """Token ids below 0 or at/above the vocabulary read the first or last
+    embedding row (the documented clamp): the same logits as the clamped ids."""
+    import torch
+    b = tiny_batch()
+    mw = make_model_weights(TINY, 1, VOCAB)
+    ids = b.token_ids(VOCAB)
+    bad = ids.copy()
+    bad[::3] = -5
+    bad[1::3] = VOCAB + 17
+    clamped = np.clip(bad, 0, VOCAB - 1).astype(np.int32)
+    dm = _device_model(b, mw, b.n_tokens, len(b.requests))
+    _, l_bad = dm.run(_reqs(b), bad)
+    torch.cuda.synchronize()
+    got_bad = l_bad.cpu().numpy()
+    _, l_ok = dm.run(_reqs(b), clamped)
+    torch.cuda.synchronize()
+    assert np.array_equal(got_bad, l_ok.cpu().numpy())
