@@ -92,9 +92,13 @@ def predict_latency(coef, n_q_heads: int, n_kv_heads: int, head_dim: int, reques
 
 
 def select_chunk(coef, n_q_heads: int, n_kv_heads: int, head_dim: int, decode_contexts, deadlines_ms,
-                 now_ms: float, chunk_context: int, max_chunk: int, granularity: int) -> Tuple[int, float]:
+                 now_ms: float, chunk_context: int, max_chunk: int, granularity: int,
+                 margin: float = 0.0) -> Tuple[int, float]:
     """Largest candidate chunk (multiples of granularity below max_chunk, or
-    max_chunk) whose batch's predicted latency is within the slack; 0 if none."""
+    max_chunk) whose batch's predicted latency, scaled by (1 + margin), is
+    within the slack; 0 if none. Section 3.3 asks for a chunk that violates no
+    deadline; the predictor errs, so a caller covers its error with the
+    margin (the relative under-prediction it is prepared to absorb)."""
     slack = min((d - now_ms for d in deadlines_ms), default=math.inf)
     decodes = [(1, int(x)) for x in decode_contexts]
 
@@ -104,6 +108,6 @@ def select_chunk(coef, n_q_heads: int, n_kv_heads: int, head_dim: int, decode_co
     cands = sorted({c for c in range(granularity, max_chunk + 1, granularity)} | ({max_chunk} if max_chunk else set()))
     best = 0
     for c in cands:  # every candidate, no early exit
-        if pred(c) <= slack:
+        if pred(c) * (1.0 + margin) <= slack:
             best = max(best, c)
     return best, pred(best)
