@@ -26,6 +26,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM = 8.0e12       # MI355X HBM3E bytes/s
 PEAK_BF16 = 2.5e15      # MI355X dense bf16 MFMA flop/s
 RIDGE = PEAK_BF16 / PEAK_HBM
+SETTLE_MS = 150.0       # continuous iterations before the measured passes
 
 
 def log(msg: str) -> None:
@@ -34,23 +35,36 @@ def log(msg: str) -> None:
 
 def kernel_work(shape, requests, out_f32=True):
     """Algorithmic (flops, HBM bytes) of each kernel for one iteration: the
-    operands each must read and the results it must write once, nothing more."""
+    layer's algorithmic work (layer_work) split over the kernels that must do
+    it. Bytes are what the method must move -- bf16 weights once, the cached
+    and new K/V read once per (request, kv head), the new K/V written, x_in
+    (bf16) and y -- and nothing an implementation adds: the intermediates q,
+    the attention output, h2, the normed activations and the SwiGLU product
+    are not counted. Flops: 2 T N K per GEMM, 4 n_q hd per unmasked (query,
+    key) pair for attention, 4 T H per RMSNorm."""
     T = sum(c for c, _ in requests)
     H, nq, nkv, hd, F = shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn_dim
     qd, qkv_n = nq * hd, (nq + 2 * nkv) * hd
     pairs = sum(c * x + c * (c + 1) / 2 for c, x in requests)
     kv_tok = sum(c + x for c, x in requests)
+    kv_b = 2.0 * 2 * nkv * hd  # bf16 K and V of one token
     yb = 4 if out_f32 else 2
     return {
-        "rmsnorm_attn": (4.0 * T * H, 2.0 * T * H + 2 * H + 2.0 * T * H),
+        "rmsnorm_attn": (4.0 * T * H, 2.0 * T * H + 2.0 * H),                 # x_in, g_attn
         # QKV projection with RoPE and the paged K/V scatter in its epilogue
-        "gemm_qkv": (2.0 * T * H * qkv_n, 2.0 * (H * qkv_n + T * H + T * qkv_n)),
-        "attention": (4.0 * nq * hd * pairs, 2.0 * 2 * nkv * hd * kv_tok + 2.0 * T * qd * 2),
-        "gemm_o": (2.0 * T * qd * H, 2.0 * H * qd + 2.0 * T * qd + 2.0 * T * H + 4.0 * T * H),
-        "rmsnorm_ffn": (4.0 * T * H, 4.0 * T * H + 2 * H + 2.0 * T * H),
-        "gemm_gate_up": (2.0 * T * H * 2 * F, 2.0 * 2 * F * H + 2.0 * T * H + 2.0 * T * F),
-        "gemm_down": (2.0 * T * F * H, 2.0 * H * F + 2.0 * T * F + 4.0 * T * H + yb * T * H),
+        "gemm_qkv": (2.0 * T * H * qkv_n, 2.0 * H * qkv_n + kv_b * T),        # W_qkv, new K/V written
+        "attention": (4.0 * nq * hd * pairs, kv_b * kv_tok),                   # cached + new K/V read
+        "attn_merge": (0.0, 0.0),
+        "gemm_o": (2.0 * T * qd * H, 2.0 * H * qd),                            # W_o
+        "rmsnorm_ffn": (4.0 * T * H, 2.0 * H),                                 # g_ffn
+        "gemm_gate_up": (2.0 * T * H * 2 * F, 2.0 * 2 * F * H),               # W_gate_up
+        "gemm_down": (2.0 * T * F * H, 2.0 * H * F + yb * T * H),             # W_down, y
     }
+
+
+def roofline_time_s(work):
+    """Sum over kernels of max(flops / bf16 peak, bytes / HBM peak)."""
+    return sum(max(f / PEAK_BF16, b / PEAK_HBM) for f, b in work.values())
 
 
 def layer_work(shape, requests, out_f32=True):
@@ -102,13 +116,25 @@ def measured_traffic(kernel, workload):
         return None
 
 
-def cpu_baseline(batch, weights_bits, min_cpu_s=10.0, max_wall_s=40.0):
-    """The oracle (fp64 NumPy) on the same batch, host cores, timed. The
-    batch is run repeatedly until at least min_cpu_s of oracle time has been
-    measured (seeding each run's cached context is not timed)."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def time_oracle(batch, weights_bits, min_cpu_s, max_wall_s, max_runs=None, w64=None):
+    """Run the oracle (fp64 NumPy) on a batch repeatedly until min_cpu_s of
+    oracle time (or max_wall_s of wall time, or max_runs runs) has passed;
+    seeding each run's cached context is not timed. Returns the per-run
+    seconds."""
     import oracle
     shape = batch.shape
-    w64 = oracle.weights_to_f64(weights_bits)
+    w64 = oracle.weights_to_f64(weights_bits) if w64 is None else w64
     x = oracle.bf16_bits_to_f64(batch.x_in())
     prior = {r: tuple(oracle.bf16_bits_to_f64(a) for a in batch.prior_kv(r))
              for r, q in enumerate(batch.requests) if q.context_len}
@@ -121,19 +147,89 @@ def cpu_baseline(batch, weights_bits, min_cpu_s=10.0, max_wall_s=40.0):
         t0 = time.perf_counter()
         oracle.layer_forward(w64, shape, cache, batch.requests, x)
         times.append(time.perf_counter() - t0)
-        if sum(times) >= min_cpu_s or time.perf_counter() - t_start > max_wall_s:
+        if (sum(times) >= min_cpu_s or time.perf_counter() - t_start > max_wall_s
+                or (max_runs and len(times) >= max_runs)):
             break
+    return times
+
+
+def blas_threads():
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
     try:
         from threadpoolctl import threadpool_info
         threads = max(int(i.get("num_threads", 0)) for i in threadpool_info()) or threads
     except Exception:
         pass
+    return threads
+
+
+def cpu_baseline(batch, weights_bits, min_cpu_s=10.0, max_wall_s=40.0):
+    """The oracle (fp64 NumPy) on the same batch, on the host's cores, timed
+    (repeated until min_cpu_s of oracle time), and once more on one thread."""
+    import oracle
+    w64 = oracle.weights_to_f64(weights_bits)
+    times = time_oracle(batch, weights_bits, min_cpu_s, max_wall_s, w64=w64)
+    one = None
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            t1 = time_oracle(batch, weights_bits, 0.0, max_wall_s, max_runs=1, w64=w64)
+        one = {"value": batch.n_tokens / t1[0], "unit": "tokens/s", "cores": 1, "seconds": round(t1[0], 2)}
+    except Exception:
+        pass
     total = float(sum(times))
-    return {"value": batch.n_tokens * len(times) / total, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+    return {"value": batch.n_tokens * len(times) / total, "unit": "tokens/s", "cores": blas_threads(),
+            "kind": "oracle", "cpu_model": cpu_model(), "one_thread": one,
             "sample": f"the bench batch ({batch.n_tokens} tokens, {len(batch.requests)} requests) run "
-                      f"{len(times)} times, {total:.1f} s of fp64 NumPy oracle time; "
-                      f"cached-context seeding not timed"}
+                      f"{len(times)} times, {total:.1f} s of fp64 NumPy oracle time (cached-context seeding not "
+                      f"timed); one_thread: one more run on a single BLAS thread"}
+
+
+def cpu_baselines():
+    """The oracle on the host's cores over the configurations of the layer's
+    workloads (one JSON line per configuration, then a summary line): the
+    tiny layer, the 8B bench batch (also on one thread), the 8B multi-request
+    batch, the sweep's corner cells (chunk 128 / 2048 x 0 / 256 decodes), the
+    70B layer (one run). Median of 3 runs, except the 70B layer. A reported
+    baseline of the oracle as it stands, not a target."""
+    from threadpoolctl import threadpool_limits
+    from hb_workloads import (LLAMA3_70B, LLAMA3_8B, TINY, llama70b_batch, llama8b_batch, make_weights, multi_batch,
+                              sweep_batch, tiny_batch)
+    import oracle
+    cases = [("tiny: chunk 64 at 128 + 8 decodes at 256", TINY, tiny_batch, 3, None),
+             ("llama3-8b: chunk 512 + 64 decodes (bench batch)", LLAMA3_8B, llama8b_batch, 3, None),
+             ("llama3-8b: chunk 512 + 64 decodes (bench batch), one thread", LLAMA3_8B, llama8b_batch, 1, 1),
+             ("llama3-8b: 4 chunks + 256 decodes", LLAMA3_8B, multi_batch, 3, None)]
+    for c in (128, 2048):
+        for n in (0, 256):
+            cases.append((f"llama3-8b sweep: chunk {c} + {n} decodes", LLAMA3_8B,
+                          (lambda c=c, n=n: sweep_batch(c, n)), 3, None))
+    cases.append(("llama3-70b: chunk 2048 at 30720 + 32 decodes at 32768", LLAMA3_70B, llama70b_batch, 1, None))
+    weights = {}
+    out = []
+    for name, shape, mk, runs, threads in cases:
+        if shape.name not in weights:
+            weights.clear()
+            weights[shape.name] = oracle.weights_to_f64(make_weights(shape))
+        b = mk()
+        log(f"cpu baseline: {name}")
+        if threads:
+            with threadpool_limits(limits=threads):
+                t = time_oracle(b, None, 1e30, 1e30, max_runs=runs, w64=weights[shape.name])
+        else:
+            t = time_oracle(b, None, 1e30, 1e30, max_runs=runs, w64=weights[shape.name])
+        fl, _ = layer_work(shape, [(q.chunk_len, q.context_len) for q in b.requests])
+        med = float(np.median(t))
+        rec = {"config": name, "tokens": b.n_tokens, "requests": len(b.requests), "runs": len(t),
+               "median_s": round(med, 3), "tokens_per_s": round(b.n_tokens / med, 1),
+               "gflops": round(fl / med / 1e9, 1), "threads": threads or blas_threads()}
+        print(json.dumps(rec), flush=True)
+        out.append(rec)
+    print(json.dumps({"cpu_model": cpu_model(), "nproc": os.cpu_count(),
+                      "affinity": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None,
+                      "blas_threads": blas_threads(), "oracle": "fp64 NumPy (oracle/layer.py)",
+                      "configs": out}), flush=True)
+    return 0
 
 
 def copy_calibration(nbytes=1 << 30, reps=3):
@@ -241,15 +337,17 @@ def fit_and_validate_latency_model(hb, dl, shape, mixes, median_ms, iters):
     errs = [abs(v["predicted_ms"] / v["measured_ms"] - 1) for v in validation]
     ctx = [int(c) for c in rng.integers(512, 4096, 64)]
     picks, sel_batches = [], []
+    margin = model.fit_max_under
     for slack in (0.45, 0.6, 0.9):
-        c, p = hb.hb_select_chunk(model, dl.cfg, ctx, [100.0 + slack] * 64, 100.0, 2048, 4096, 32)
+        c, p = hb.hb_select_chunk(model, dl.cfg, ctx, [100.0 + slack] * 64, 100.0, 2048, 4096, 32, margin)
         picks.append((slack, c, p))
         sel_batches.append(make_batch(shape, [(max(c, 1), 2048)] + [(1, x) for x in ctx], 50))
     sel_meas = timed(sel_batches)
     return {"features": ["1", "T/1e3", "KV GB read", "attention TFLOP vs cached context",
                          "attention TFLOP within new tokens"],
             "coef_ms": [round(c, 5) for c in model.coef], "fit_cells": model.n_cells,
-            "fit_rel_rms": round(model.fit_rel_rms, 4), "validation": validation,
+            "fit_rel_rms": round(model.fit_rel_rms, 4), "fit_max_under": round(model.fit_max_under, 4),
+            "selector_margin": round(margin, 4), "validation": validation,
             "validation_mape": round(float(np.mean(errs)), 4), "validation_max_err": round(float(np.max(errs)), 4),
             "selector": [{"decodes": 64, "chunk_context": 2048, "slack_ms": s, "chunk": c,
                           "predicted_ms": round(p, 4), "measured_ms": round(float(m), 4)}
@@ -435,6 +533,8 @@ def main() -> int:
                     help="only run one cell ('C,D', '70b' or 'multi') --warmup + --steps times (counter passes) and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration) and exit")
+    ap.add_argument("--cpu-baselines", action="store_true",
+                    help="only time the CPU oracle over the workload configurations (no GPU) and exit")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the hybrid-batch layer runs on a single MI355X; "
@@ -442,6 +542,8 @@ def main() -> int:
         return 2
     if a.copy_calibration:
         return copy_calibration()
+    if a.cpu_baselines:
+        return cpu_baselines()
     if a.counters_cell:
         return counters_cell(a.counters_cell, a.steps, a.warmup)
 
@@ -474,13 +576,20 @@ def main() -> int:
 
     work = kernel_work(shape, [(c, xx) for c, xx, _ in reqs])
 
+    # The GPU runs its first tens of milliseconds of work after an idle spell
+    # at lower clocks (about 40 ms of iterations to reach steady state on
+    # MI355X). Steady serving keeps it busy, so the measured passes start
+    # after SETTLE_MS of continuous iterations, with no host gap longer than
+    # a synchronisation before the timed region.
+    n_settle = max(a.steps, int(np.ceil(SETTLE_MS / 0.4)))
+    for _ in range(n_settle):
+        dl.run(reqs, x, hb.HB_OUT_F32, y)
     # per-kernel breakdown (every launch bracketed by events) picks the dominant kernel
+    n_breakdown = max(a.steps, 50)
     hb.hb_set_kernel_timing(dl.layer, True)
-    hb.hb_kernel_times(dl.layer, reset=True)
-    for _ in range(a.steps):
+    for _ in range(n_breakdown):
         dl.run(reqs, x, hb.HB_OUT_F32, y)
     breakdown = hb.hb_kernel_times(dl.layer, reset=True)
-    hb.hb_set_kernel_timing(dl.layer, False)
     kernels = {}
     for name, (tot, n) in breakdown.items():
         if n == 0:
@@ -489,18 +598,17 @@ def main() -> int:
         fl, by = work.get(name, (0.0, 0.0))
         kernels[name] = {"avg_ms": round(avg_ms, 5), "launches": n,
                          "tflops": round(fl / (avg_ms * 1e-3) / 1e12, 2) if fl else None,
-                         "gbps": round(by / (avg_ms * 1e-3) / 1e9, 1) if by else None}
+                         "gbps": round(by / (avg_ms * 1e-3) / 1e9, 1) if by else None,
+                         "roofline_frac": round(max(fl / PEAK_BF16, by / PEAK_HBM) / (avg_ms * 1e-3), 4)}
     dom = max(kernels, key=lambda k: kernels[k]["avg_ms"] * kernels[k]["launches"])
 
-    # timed region: exactly `steps` iterations; HIP events on the layer's stream
-    # bracket only the dominant kernel's launches. The warm-up iterations are
-    # repeated in this configuration first, so the timed steps do not start
-    # right after the breakdown pass's per-launch events.
+    # timed region: W warm-up iterations, then exactly `steps` iterations;
+    # HIP events on the layer's stream bracket only the dominant kernel's
+    # launches (two event records per step)
     hb.hb_set_kernel_timing(dl.layer, [dom])
     for _ in range(a.warmup):
         dl.run(reqs, x, hb.HB_OUT_F32, y)
-    torch.cuda.synchronize()
-    hb.hb_kernel_times(dl.layer, reset=True)
+    hb.hb_kernel_times(dl.layer, reset=True)  # synchronises; drops the warm-up's events
     t0 = time.perf_counter()
     for _ in range(a.steps):
         dl.run(reqs, x, hb.HB_OUT_F32, y)
@@ -613,10 +721,16 @@ def main() -> int:
         "layer_roofline": {"algorithmic_gflop": round(flops / 1e9, 2), "algorithmic_mb": round(bytes_ / 1e6, 1),
                            "mfma_frac": round(flops / step_s / PEAK_BF16, 4),
                            "hbm_frac": round(bytes_ / step_s / PEAK_HBM, 4),
-                           "roofline_time_us": round(max(flops / PEAK_BF16, bytes_ / PEAK_HBM) * 1e6, 1)},
+                           "roofline_time_us": round(roofline_time_s(work) * 1e6, 1),
+                           "frac": round(roofline_time_s(work) / step_s, 4),
+                           "note": "roofline time = sum over kernels of max(flops / bf16 peak, bytes / HBM peak); "
+                                   "frac = roofline time / ms_per_step"},
         "roofline": roof,
         "kernels": kernels,
-        "kernels_note": "per-kernel averages from a separate pass with every launch bracketed by events",
+        "kernels_note": "per-kernel averages from a separate pass with every launch bracketed by events; "
+                        "bytes and flops are each kernel's share of the layer's algorithmic work",
+        "passes": {"settle_steps": n_settle, "breakdown_steps": n_breakdown, "warmup": a.warmup,
+                   "timed_steps": a.steps},
         "cpu_baseline": cpu,
         "gates": gates,
         "gates_note": "per-kernel averages with every launch bracketed by events; algorithmic work as for roofline; "

@@ -60,7 +60,12 @@ typedef struct hb_layer hb_layer; /* opaque, library-owned */
  *   rope_theta    RoPE base; angle of pair j at position p is p*theta^(-2j/head_dim)
  *   rms_eps       RMSNorm epsilon
  *   max_batch_tokens  largest T = sum of chunk_len accepted by hb_run_iteration
- *   max_requests      largest number of requests in one batch */
+ *   max_requests      largest number of requests in one batch
+ * Size limit: the GEMMs address each operand through a buffer window of
+ * 2^31 - 16 bytes, so every weight matrix ((n_q + 2 n_kv) head_dim x H,
+ * H x n_q head_dim, 2F x H, H x F) and every activation operand
+ * ((max_batch_tokens + 512) rows of H, n_q head_dim or F bf16 values) must
+ * fit in it; a configuration that does not is HB_ERR_UNSUPPORTED. */
 typedef struct {
   int32_t hidden, n_q_heads, n_kv_heads, head_dim, ffn_dim, kv_block_size;
   float rope_theta, rms_eps;
@@ -94,8 +99,9 @@ typedef struct {
  * selects the null stream). Allocates the library's workspace for
  * max_batch_tokens / max_requests on the current device.
  * Errors: HB_ERR_INVALID (null pointer, non-positive size),
- * HB_ERR_UNSUPPORTED (shape outside the limits above), HB_ERR_OOM, HB_ERR_HIP.
- * On error *out is set to NULL. */
+ * HB_ERR_UNSUPPORTED (shape outside the limits above, including the 2 GiB
+ * operand window), HB_ERR_OOM, HB_ERR_HIP. Configuration errors are found
+ * before any HIP call. On error *out is set to NULL. */
 hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w,
                           const hb_kv_pool* pool, void* hip_stream, hb_layer** out);
 
@@ -177,7 +183,9 @@ typedef struct {
  * Section 3.6): for every mix m and chunk size c, synthesise a batch of one
  * c-token chunk at mix.chunk_context plus the mix's decodes, with block tables
  * drawn from a seeded permutation of the whole pool, fill the blocks it uses
- * and its input with seeded pseudo-random bf16, run `warmup` untimed
+ * and its input with seeded pseudo-random bf16 (before the first cell, run
+ * its batch untimed for 100 ms of device time, so that the GPU is at its
+ * steady clocks), run `warmup` untimed
  * iterations, then `iters` iterations each preceded by a write of a 512 MiB
  * buffer (so no data stays in the 256 MB Infinity Cache) and timed with HIP
  * events; each timed iteration is planned and its metadata uploaded before
@@ -190,7 +198,8 @@ hb_status hb_profile(hb_layer* layer, const int32_t* chunk_sizes, int32_t n_chun
                      const hb_decode_mix* mixes, int32_t n_mix, int32_t warmup, int32_t iters,
                      uint64_t seed, hb_profile_cell* out);
 
-/* Latency of given batches, timed as hb_profile times its cells: for each
+/* Latency of given batches, timed as hb_profile times its cells (the first
+ * batch first run untimed for 100 ms of device time): for each
  * batch, `warmup` untimed iterations, then `iters` iterations each after a
  * write of a 512 MiB buffer, each planned and its metadata uploaded before
  * the start event, so an interval holds the layer's kernels alone. The
@@ -222,7 +231,9 @@ hb_status hb_profile_batches(hb_layer* layer, const hb_batch_desc* batches, int3
 #define HB_LAT_FEATURES 5
 typedef struct {
   double coef[HB_LAT_FEATURES];
-  double fit_rel_rms; /* root mean square of (predicted - measured) / measured over the cells */
+  double fit_rel_rms;   /* root mean square of (predicted - measured) / measured over the cells */
+  double fit_max_under; /* largest measured / predicted - 1 over the cells (0 if none is under-predicted):
+                           the margin hb_select_chunk needs for no fitted cell to exceed its slack */
   int32_t n_cells;
 } hb_latency_model;
 
@@ -252,16 +263,19 @@ hb_status hb_predict_latency(const hb_latency_model* model, const hb_layer_confi
  * minus now_ms; with no decodes it is unbounded. The chunk is the largest
  * c in {granularity, 2 granularity, ...} below max_chunk, or max_chunk itself
  * (the rest of the prompt), whose batch -- one c-token chunk at chunk_context
- * next to the decodes -- has a predicted latency within the slack (a
- * prediction equal to the slack fits); 0 when
- * none fits or max_chunk is 0. *predicted_ms receives the predicted latency of
- * the chosen batch (decodes only when *chunk is 0). Host only. Errors:
+ * next to the decodes -- fits the slack with the caller's safety margin:
+ * predicted latency * (1 + margin) <= slack (margin >= 0 covers the model's
+ * error, e.g. model->fit_max_under, so that the chosen chunk violates no
+ * deadline as Section 3.3 requires); 0 when none fits or max_chunk is 0.
+ * *predicted_ms receives the predicted latency (without the margin) of the
+ * chosen batch (decodes only when *chunk is 0). Host only. Errors:
  * HB_ERR_INVALID (null pointer, n_decode < 0, a negative context,
- * chunk_context < 0, max_chunk < 0, granularity < 1, a NaN deadline or now_ms). */
+ * chunk_context < 0, max_chunk < 0, granularity < 1, margin < 0 or NaN, a NaN
+ * deadline or now_ms). */
 hb_status hb_select_chunk(const hb_latency_model* model, const hb_layer_config* cfg,
                           const int32_t* decode_contexts, const double* decode_deadlines_ms, int32_t n_decode,
                           double now_ms, int32_t chunk_context, int32_t max_chunk, int32_t granularity,
-                          int32_t* chunk, double* predicted_ms);
+                          double margin, int32_t* chunk, double* predicted_ms);
 
 /* Whole-model iteration: n_layers decoder layers (each an hb_layer with its
  * own weights and its own paged pool) between a token embedding and a final
@@ -273,7 +287,8 @@ hb_status hb_select_chunk(const hb_latency_model* model, const hb_layer_config* 
  *   pools   [n_layers] paged pools, all with the same num_blocks: a request's
  *           block table names the same blocks in every layer's pool
  *   embed   device bf16 [vocab][H]; g_final device bf16 [H]; lm_head device
- *           bf16 [vocab][H]; vocab % 8 == 0
+ *           bf16 [vocab][H]; vocab % 8 == 0, vocab * H * 2 bytes within the
+ *           2 GiB operand window of the layer GEMMs
  * Caller-owned; everything must outlive the model. */
 typedef struct hb_model hb_model; /* opaque, library-owned */
 typedef struct {
@@ -284,9 +299,10 @@ typedef struct {
 } hb_model_desc;
 
 /* Create a model on a HIP stream (all its layers use it). Errors as
- * hb_create_layer, and HB_ERR_INVALID for n_layers < 1, vocab < 8 or not a
- * multiple of 8, pools of different sizes, null pointers. *out is NULL on
- * error. */
+ * hb_create_layer, HB_ERR_INVALID for n_layers < 1, vocab < 8 or not a
+ * multiple of 8, pools of different sizes, null pointers, and
+ * HB_ERR_UNSUPPORTED for an LM head beyond the 2 GiB operand window; all are
+ * found before any HIP call. *out is NULL on error. */
 hb_status hb_create_model(const hb_layer_config* cfg, const hb_model_desc* desc, void* hip_stream,
                           hb_model** out);
 void hb_destroy_model(hb_model* model);
@@ -302,6 +318,9 @@ hb_layer* hb_model_layer(hb_model* model, int32_t index);
  * row); for the last row of each request, logits (device fp32
  * [n_requests][vocab], or NULL to keep them internal) and next_tokens
  * (device int32 [n_requests]: the lowest index of the largest logit).
+ * hidden_states: NULL, or device bf16 [n_layers][T][H] that receives every
+ * layer's output (layer l reads its input from slice l - 1; for per-layer
+ * checks); must not overlap the other buffers.
  * Enqueues on the model's stream and returns. Errors: those of
  * hb_run_iteration, HB_ERR_INVALID for null token_ids / next_tokens or an
  * empty batch. */
@@ -311,6 +330,7 @@ typedef struct {
   const int32_t* token_ids;
   float* logits;
   int32_t* next_tokens;
+  void* hidden_states;
 } hb_model_batch;
 hb_status hb_run_model(hb_model* model, const hb_model_batch* batch);
 
@@ -339,6 +359,29 @@ const char* hb_kernel_name(int32_t kernel);
  *   HB_STAGE_MLP   bf16 [T][F]             silu(gate) * up */
 enum { HB_STAGE_Q = 0, HB_STAGE_ATTN = 1, HB_STAGE_H2 = 2, HB_STAGE_MLP = 3 };
 hb_status hb_layer_stage(hb_layer* layer, int32_t stage, void** dev_ptr, int64_t* row_stride);
+
+/* GEMM launch plans, for tests and tuning. The four GEMMs of the layer are
+ * numbered HB_GEMM_QKV, HB_GEMM_O, HB_GEMM_GATE_UP, HB_GEMM_DOWN; a plan is a
+ * tile-shape index in [0, hb_gemm_tile_count()) (-1: the register-staged
+ * kernel used when K is not a multiple of 64) and a K split (1: none; > 1:
+ * fp32 partials summed by a second kernel that applies the epilogue). */
+enum { HB_GEMM_QKV = 0, HB_GEMM_O = 1, HB_GEMM_GATE_UP = 2, HB_GEMM_DOWN = 3, HB_GEMM_COUNT = 4 };
+int32_t hb_gemm_tile_count(void);
+
+/* The plans the library chooses for a batch of n_tokens tokens on a GPU with
+ * cu_count compute units (host only). force_tile >= 0 / force_ksplit > 0
+ * restrict the choice to one tile shape / K split as the HB_GEMM_TILE /
+ * HB_GEMM_KSPLIT environment variables do when a layer is created (testing):
+ * a forced choice that cannot run a GEMM is relaxed, the split first.
+ * tile[HB_GEMM_COUNT], ksplit[HB_GEMM_COUNT] receive the plans. Errors:
+ * HB_ERR_INVALID (null pointer, n_tokens < 1, cu_count < 1), configuration
+ * errors as hb_create_layer. */
+hb_status hb_plan_gemms(const hb_layer_config* cfg, int32_t n_tokens, int32_t cu_count, int32_t force_tile,
+                        int32_t force_ksplit, int32_t* tile, int32_t* ksplit);
+
+/* The plans of the layer's most recent iteration (0 tokens: all -1 / 0).
+ * Errors: HB_ERR_INVALID (null pointer). */
+hb_status hb_layer_gemm_plans(hb_layer* layer, int32_t* tile, int32_t* ksplit);
 
 /* Message for the last non-OK status returned on this host thread. */
 const char* hb_last_error(void);

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
+#include "hb_plan.h"
+
 namespace hb {
 
 // Per-token RoPE inputs for the QKV epilogue, written by the first RMSNorm:
@@ -28,10 +30,10 @@ void launch_rmsnorm(hipStream_t s, const void* x, bool x_f32, const uint16_t* g,
 
 enum GemmEpilogue { GEMM_STORE_BF16 = 0, GEMM_RESIDUAL = 1, GEMM_SWIGLU = 2, GEMM_QKV_ROPE = 3 };
 
-// Rows past M that a GEMM's A operand must keep readable: the LDS-pipelined
-// kernels load whole row tiles (at most 288 rows) and never store the rows
-// past M. Their B operands need N % 8 == 0 (8-row load groups).
-constexpr int kGemmPadRows = 512;
+// Rows past M that a GEMM's A operand must keep readable (kGemmPadRows, in
+// hb_plan.h): the LDS-pipelined kernels load whole row tiles (at most 288
+// rows) and never store the rows past M. Their B operands need N % 8 == 0
+// (8-row load groups). Every operand must fit kOperandWindow bytes.
 
 // C[M][N] = A[M][K] * B[N][K]^T with an epilogue:
 //   GEMM_STORE_BF16: C bf16

@@ -65,6 +65,9 @@ hb_status hb_create_model(const hb_layer_config* cfg, const hb_model_desc* md, v
     if (md->pools[l].num_blocks != md->pools[0].num_blocks)
       return fail(HB_ERR_INVALID, "layer %d pool has %d blocks, layer 0 %d", l, md->pools[l].num_blocks,
                   md->pools[0].num_blocks);
+  // the LM head is a B operand of the layer GEMM
+  st = check_window("lm_head", md->vocab, d.H);
+  if (st != HB_OK) return st;
   hb_model* m = new hb_model;
   m->cfg = *cfg;
   m->embed = static_cast<const uint16_t*>(md->embed);
@@ -135,15 +138,19 @@ hb_status hb_run_model(hb_model* m, const hb_model_batch* b) {
   m->rows_pending = true;
 
   launch_gather_rows(m->stream, m->embed, m->vocab, b->token_ids, T, H, m->x[0]);
-  int cur = 0;
-  for (hb_layer* L : m->layers) {
-    desc.x_in = m->x[cur];
-    desc.x_out = m->x[1 - cur];
-    st = hb_run_iteration(L, &desc);
+  // hidden states ping-pong between two buffers, or go to the caller's
+  // per-layer slices
+  uint16_t* hs = static_cast<uint16_t*>(b->hidden_states);
+  const uint16_t* cur = m->x[0];
+  for (size_t l = 0; l < m->layers.size(); ++l) {
+    uint16_t* next = hs ? hs + l * (size_t)T * H : m->x[(cur == m->x[0]) ? 1 : 0];
+    desc.x_in = cur;
+    desc.x_out = next;
+    st = hb_run_iteration(m->layers[l], &desc);
     if (st != HB_OK) return st;
-    cur = 1 - cur;
+    cur = next;
   }
-  launch_gather_rows(m->stream, m->x[cur], T, m->rows_dev, R, H, m->last);
+  launch_gather_rows(m->stream, cur, T, m->rows_dev, R, H, m->last);
   launch_rmsnorm(m->stream, m->last, false, m->g_final, m->normed, R, H, c.rms_eps);
 
   float* logits = b->logits ? b->logits : m->logits;

@@ -41,6 +41,21 @@ hb_status check_config(const hb_layer_config* c, Dims* d) {
   if (c->ffn_dim % 16) return fail(HB_ERR_UNSUPPORTED, "ffn_dim must be a multiple of 16 (got %d)", c->ffn_dim);
   if (c->max_batch_tokens > (1 << 20) || c->max_requests > (1 << 20))
     return fail(HB_ERR_UNSUPPORTED, "max_batch_tokens / max_requests above 2^20");
+  {
+    // every GEMM operand within the buffer window: the four weight matrices
+    // and the three activation operands (with their padding rows)
+    const int64_t H = c->hidden, F = c->ffn_dim, qd = (int64_t)c->n_q_heads * c->head_dim;
+    const int64_t qkv = (int64_t)(c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim;
+    const int64_t TA = (int64_t)c->max_batch_tokens + kGemmPadRows;
+    hb_status st = check_window("w_qkv", qkv, H);
+    if (st == HB_OK) st = check_window("w_o", H, qd);
+    if (st == HB_OK) st = check_window("w_gate_up", 2 * F, H);
+    if (st == HB_OK) st = check_window("w_down", H, F);
+    if (st == HB_OK) st = check_window("normed activations (max_batch_tokens + 512 rows)", TA, H);
+    if (st == HB_OK) st = check_window("attention output (max_batch_tokens + 512 rows)", TA, qd);
+    if (st == HB_OK) st = check_window("SwiGLU activations (max_batch_tokens + 512 rows)", TA, F);
+    if (st != HB_OK) return st;
+  }
   d->H = c->hidden;
   d->nq = c->n_q_heads;
   d->nkv = c->n_kv_heads;
@@ -55,6 +70,13 @@ hb_status check_config(const hb_layer_config* c, Dims* d) {
   d->eps = c->rms_eps;
   d->max_T = c->max_batch_tokens;
   d->max_R = c->max_requests;
+  return HB_OK;
+}
+
+hb_status check_window(const char* what, int64_t rows, int64_t cols) {
+  if (rows * cols * 2 > kOperandWindow)
+    return fail(HB_ERR_UNSUPPORTED, "%s: %lld x %lld bf16 values exceed the %lld-byte GEMM operand window", what,
+                (long long)rows, (long long)cols, (long long)kOperandWindow);
   return HB_OK;
 }
 

@@ -28,7 +28,17 @@ struct Dims {
   int max_T = 0, max_R = 0;
 };
 
+// Bytes of an operand the GEMMs can address: each operand is read through a
+// raw buffer resource of this many records (and 32-bit byte offsets), so
+// nothing past it may be needed. Rows past M that the GEMMs read from their
+// activation operands (whole row tiles): kGemmPadRows.
+constexpr int64_t kOperandWindow = 0x7FFFFFF0;
+constexpr int kGemmPadRows = 512;
+
 hb_status check_config(const hb_layer_config* cfg, Dims* d);
+
+// HB_ERR_UNSUPPORTED unless rows x cols bf16 values fit the operand window.
+hb_status check_window(const char* what, int64_t rows, int64_t cols);
 
 // Attention work over the key positions [kv_begin, kv_end) of one request
 // and kv head: a wave item covers 16 query columns (P positions x G heads), a

@@ -172,6 +172,13 @@ extern "C" hb_status hb_fit_latency_model(const hb_layer_config* cfg, const int3
   if (!std::isfinite(best_res)) return fail(HB_ERR_INVALID, "hb_fit_latency_model: no non-negative fit");
   std::memcpy(out->coef, best, sizeof(best));
   out->fit_rel_rms = std::sqrt(best_res / rows);
+  // largest under-prediction: measured / predicted - 1 over the cells
+  double under = 0;
+  for (int r = 0; r < rows; ++r) {
+    const double pred = dot(&raw[(size_t)r * NF], best);
+    if (pred > 0) under = std::fmax(under, cells[r].median_ms / pred - 1.0);
+  }
+  out->fit_max_under = under;
   out->n_cells = rows;
   return HB_OK;
 }
@@ -189,13 +196,14 @@ extern "C" hb_status hb_predict_latency(const hb_latency_model* model, const hb_
 extern "C" hb_status hb_select_chunk(const hb_latency_model* model, const hb_layer_config* cfg,
                                      const int32_t* decode_contexts, const double* decode_deadlines_ms,
                                      int32_t n_decode, double now_ms, int32_t chunk_context, int32_t max_chunk,
-                                     int32_t granularity, int32_t* chunk, double* predicted_ms) {
+                                     int32_t granularity, double margin, int32_t* chunk, double* predicted_ms) {
   if (!model || !check_cfg(cfg) || !chunk || !predicted_ms || n_decode < 0 ||
       (n_decode > 0 && (!decode_contexts || !decode_deadlines_ms)))
     return fail(HB_ERR_INVALID, "hb_select_chunk: null pointer or bad size");
-  if (chunk_context < 0 || max_chunk < 0 || granularity < 1 || std::isnan(now_ms))
-    return fail(HB_ERR_INVALID, "hb_select_chunk: chunk_context %d, max_chunk %d, granularity %d", chunk_context,
-                max_chunk, granularity);
+  if (chunk_context < 0 || max_chunk < 0 || granularity < 1 || std::isnan(now_ms) || !(margin >= 0))
+    return fail(HB_ERR_INVALID, "hb_select_chunk: chunk_context %d, max_chunk %d, granularity %d, margin %g",
+                chunk_context, max_chunk, granularity, margin);
+  const double scale = 1.0 + margin;
   double slack = std::numeric_limits<double>::infinity();
   for (int i = 0; i < n_decode; ++i) {
     if (decode_contexts[i] < 0 || std::isnan(decode_deadlines_ms[i]))
@@ -219,13 +227,13 @@ extern "C" hb_status hb_select_chunk(const hb_latency_model* model, const hb_lay
   const int top = max_chunk / granularity * granularity;
   if (max_chunk > 0) {
     const double full = predict(max_chunk);
-    if (full <= slack) {
+    if (full * scale <= slack) {
       best = max_chunk;
       best_ms = full;
     } else {
       for (int c = (top == max_chunk ? top - granularity : top); c >= granularity; c -= granularity) {
         const double t = predict(c);
-        if (t <= slack) {
+        if (t * scale <= slack) {
           best = c;
           best_ms = t;
           break;

@@ -420,8 +420,8 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
     }
     bo[j] = 2u * (uint32_t)brow * (uint32_t)a.ldb;
   }
-  const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(a.A + k_begin, 0x7FFFFFF0u);
-  const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(a.B + k_begin, 0x7FFFFFF0u);
+  const __amdgpu_buffer_rsrc_t ra = buffer_rsrc(a.A + k_begin, (uint32_t)kOperandWindow);
+  const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(a.B + k_begin, (uint32_t)kOperandWindow);
 
   f32x4 acc[TM][TN];
 #pragma unroll

@@ -139,12 +139,14 @@ class DeviceModel:
         hb.hb_append_kv(self.model.layer(layer), block_table, context_len, k, v)
         _torch().cuda.current_stream().synchronize()  # k, v are freed on return
 
-    def run(self, requests: Sequence[Tuple[int, int, np.ndarray]], token_ids: np.ndarray, keep_logits: bool = True):
-        """Enqueue one model iteration; returns (next_tokens int32 [R], logits fp32 [R][vocab] or None)."""
+    def run(self, requests: Sequence[Tuple[int, int, np.ndarray]], token_ids: np.ndarray, keep_logits: bool = True,
+            hidden_states=None):
+        """Enqueue one model iteration; returns (next_tokens int32 [R], logits fp32 [R][vocab] or None).
+        hidden_states: None, or a device bf16 [n_layers][T][H] tensor that receives every layer's output."""
         torch = _torch()
         ids = torch.from_numpy(np.ascontiguousarray(token_ids, dtype=np.int32)).to(self.device)
         nxt = torch.empty(len(requests), dtype=torch.int32, device=self.device)
         logits = torch.empty((len(requests), self.vocab), dtype=torch.float32, device=self.device) if keep_logits else None
-        hb.hb_run_model(self.model, requests, ids, nxt, logits)
+        hb.hb_run_model(self.model, requests, ids, nxt, logits, hidden_states)
         self._ids = ids  # alive until the caller synchronises
         return nxt, logits

@@ -18,11 +18,14 @@ HB_OUT_F32, HB_OUT_BF16 = 0, 1
 (HB_K_RMSNORM_ATTN, HB_K_GEMM_QKV, HB_K_ATTENTION, HB_K_ATTN_MERGE, HB_K_GEMM_O,
  HB_K_RMSNORM_FFN, HB_K_GEMM_GATE_UP, HB_K_GEMM_DOWN, HB_K_COUNT) = range(9)
 HB_STAGE_Q, HB_STAGE_ATTN, HB_STAGE_H2, HB_STAGE_MLP = range(4)
+HB_GEMM_QKV, HB_GEMM_O, HB_GEMM_GATE_UP, HB_GEMM_DOWN, HB_GEMM_COUNT = range(5)
+GEMM_NAMES = ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down")
 
 EXPORTED = ("hb_create_layer", "hb_destroy_layer", "hb_append_kv", "hb_run_iteration", "hb_validate_batch",
             "hb_profile", "hb_profile_batches", "hb_latency_features", "hb_fit_latency_model", "hb_predict_latency", "hb_select_chunk",
             "hb_create_model", "hb_destroy_model", "hb_model_layer", "hb_run_model",
-            "hb_set_kernel_timing", "hb_kernel_times", "hb_kernel_name", "hb_layer_stage", "hb_last_error")
+            "hb_set_kernel_timing", "hb_kernel_times", "hb_kernel_name", "hb_layer_stage", "hb_last_error",
+            "hb_gemm_tile_count", "hb_plan_gemms", "hb_layer_gemm_plans")
 HB_LAT_FEATURES = 5
 
 
@@ -60,7 +63,8 @@ class hb_profile_cell(C.Structure):
 
 
 class hb_latency_model(C.Structure):
-    _fields_ = [("coef", C.c_double * HB_LAT_FEATURES), ("fit_rel_rms", C.c_double), ("n_cells", C.c_int32)]
+    _fields_ = [("coef", C.c_double * HB_LAT_FEATURES), ("fit_rel_rms", C.c_double), ("fit_max_under", C.c_double),
+                ("n_cells", C.c_int32)]
 
 
 class hb_model_desc(C.Structure):
@@ -71,7 +75,7 @@ class hb_model_desc(C.Structure):
 
 class hb_model_batch(C.Structure):
     _fields_ = [("n_requests", C.c_int32), ("requests", C.POINTER(hb_request)), ("token_ids", C.c_void_p),
-                ("logits", C.c_void_p), ("next_tokens", C.c_void_p)]
+                ("logits", C.c_void_p), ("next_tokens", C.c_void_p), ("hidden_states", C.c_void_p)]
 
 
 class HBError(RuntimeError):
@@ -125,7 +129,7 @@ def load() -> C.CDLL:
     lib.hb_predict_latency.restype = st
     lib.hb_select_chunk.argtypes = [C.POINTER(hb_latency_model), C.POINTER(hb_layer_config), C.POINTER(C.c_int32),
                                     C.POINTER(C.c_double), C.c_int32, C.c_double, C.c_int32, C.c_int32, C.c_int32,
-                                    C.POINTER(C.c_int32), C.POINTER(C.c_double)]
+                                    C.c_double, C.POINTER(C.c_int32), C.POINTER(C.c_double)]
     lib.hb_select_chunk.restype = st
     lib.hb_create_model.argtypes = [C.POINTER(hb_layer_config), C.POINTER(hb_model_desc), C.c_void_p,
                                     C.POINTER(C.c_void_p)]
@@ -146,6 +150,13 @@ def load() -> C.CDLL:
     lib.hb_layer_stage.restype = st
     lib.hb_last_error.argtypes = []
     lib.hb_last_error.restype = C.c_char_p
+    lib.hb_gemm_tile_count.argtypes = []
+    lib.hb_gemm_tile_count.restype = C.c_int32
+    lib.hb_plan_gemms.argtypes = [C.POINTER(hb_layer_config), C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                  C.POINTER(C.c_int32), C.POINTER(C.c_int32)]
+    lib.hb_plan_gemms.restype = st
+    lib.hb_layer_gemm_plans.argtypes = [C.c_void_p, C.POINTER(C.c_int32), C.POINTER(C.c_int32)]
+    lib.hb_layer_gemm_plans.restype = st
     _lib = lib
     return lib
 
@@ -237,12 +248,13 @@ def hb_destroy_model(model: Model) -> None:
 
 
 def hb_run_model(model: Model, requests: Sequence[Tuple[int, int, Iterable[int]]], token_ids, next_tokens,
-                 logits=None) -> None:
+                 logits=None, hidden_states=None) -> None:
     """token_ids: device int32 [T]; next_tokens: device int32 [n_requests];
-    logits: device fp32 [n_requests][vocab] or None."""
+    logits: device fp32 [n_requests][vocab] or None; hidden_states: device
+    bf16 [n_layers][T][H] (every layer's output) or None."""
     d, keep = _desc(requests, 0, 0, HB_OUT_BF16)
     b = hb_model_batch(len(requests), d.requests, C.c_void_p(_ptr(token_ids)), C.c_void_p(_ptr(logits)),
-                       C.c_void_p(_ptr(next_tokens)))
+                       C.c_void_p(_ptr(next_tokens)), C.c_void_p(_ptr(hidden_states)))
     _check(load().hb_run_model(model.handle, C.byref(b)))
 
 
@@ -280,13 +292,31 @@ def hb_append_kv(layer: Layer, block_table, context_len: int, k, v) -> None:
                                C.c_void_p(_ptr(k)), C.c_void_p(_ptr(v))))
 
 
+# hb_request as a NumPy record: the request array is filled with array
+# operations instead of one ctypes object per request
+_REQ_DTYPE = np.dtype({"names": ["chunk_len", "context_len", "block_table", "n_blocks"],
+                       "formats": [np.int32, np.int32, np.uintp, np.int32],
+                       "offsets": [hb_request.chunk_len.offset, hb_request.context_len.offset,
+                                   hb_request.block_table.offset, hb_request.n_blocks.offset],
+                       "itemsize": C.sizeof(hb_request)})
+
+
 def _desc(requests: Sequence[Tuple[int, int, Iterable[int]]], x_in_ptr: int, x_out_ptr: int, out_dtype: int):
+    n = len(requests)
     tables = [_i32(bt) for (_, _, bt) in requests]
-    arr = (hb_request * max(1, len(requests)))()
-    for i, ((c, x, _), bt) in enumerate(zip(requests, tables)):
-        arr[i] = hb_request(int(c), int(x), bt.ctypes.data_as(C.POINTER(C.c_int32)), len(bt))
-    d = hb_batch_desc(len(requests), arr, C.c_void_p(x_in_ptr), C.c_void_p(x_out_ptr), int(out_dtype))
-    return d, (tables, arr)
+    flat = np.concatenate(tables) if n else np.zeros(1, np.int32)
+    lens = np.fromiter((len(bt) for bt in tables), dtype=np.int64, count=n)
+    rec = np.zeros(max(1, n), dtype=_REQ_DTYPE)
+    if n:
+        cx = np.array([(r[0], r[1]) for r in requests], dtype=np.int64).reshape(n, 2)
+        rec["chunk_len"][:n] = cx[:, 0]
+        rec["context_len"][:n] = cx[:, 1]
+        starts = np.concatenate([[0], np.cumsum(lens)[:-1]])
+        rec["block_table"][:n] = flat.ctypes.data + 4 * starts
+        rec["n_blocks"][:n] = lens
+    arr = rec.ctypes.data_as(C.POINTER(hb_request))
+    d = hb_batch_desc(n, arr, C.c_void_p(x_in_ptr), C.c_void_p(x_out_ptr), int(out_dtype))
+    return d, (flat, rec, arr)
 
 
 def hb_run_iteration(layer: Layer, requests: Sequence[Tuple[int, int, Iterable[int]]], x_in, x_out,
@@ -394,14 +424,14 @@ def hb_predict_latency(model: hb_latency_model, cfg: hb_layer_config, requests: 
 
 def hb_select_chunk(model: hb_latency_model, cfg: hb_layer_config, decode_contexts: Sequence[int],
                     decode_deadlines_ms: Sequence[float], now_ms: float, chunk_context: int, max_chunk: int,
-                    granularity: int) -> Tuple[int, float]:
+                    granularity: int, margin: float = 0.0) -> Tuple[int, float]:
     ctx = _i32(decode_contexts)
     dl = np.ascontiguousarray(decode_deadlines_ms, dtype=np.float64)
     chunk, ms = C.c_int32(), C.c_double()
     _check(load().hb_select_chunk(C.byref(model), C.byref(cfg), ctx.ctypes.data_as(C.POINTER(C.c_int32)),
                                   dl.ctypes.data_as(C.POINTER(C.c_double)), len(ctx), float(now_ms),
-                                  int(chunk_context), int(max_chunk), int(granularity), C.byref(chunk),
-                                  C.byref(ms)))
+                                  int(chunk_context), int(max_chunk), int(granularity), float(margin),
+                                  C.byref(chunk), C.byref(ms)))
     return chunk.value, ms.value
 
 
@@ -428,6 +458,25 @@ def hb_kernel_times(layer: Layer, reset: bool = False) -> Dict[str, Tuple[float,
 
 def hb_kernel_name(k: int) -> str:
     return load().hb_kernel_name(int(k)).decode()
+
+
+def hb_gemm_tile_count() -> int:
+    return int(load().hb_gemm_tile_count())
+
+
+def hb_plan_gemms(cfg: hb_layer_config, n_tokens: int, cu_count: int, force_tile: int = -1,
+                  force_ksplit: int = 0) -> List[Tuple[int, int]]:
+    """(tile, ksplit) of the QKV, O, gate/up and down GEMMs for a batch of n_tokens."""
+    t, k = (C.c_int32 * HB_GEMM_COUNT)(), (C.c_int32 * HB_GEMM_COUNT)()
+    _check(load().hb_plan_gemms(C.byref(cfg), int(n_tokens), int(cu_count), int(force_tile), int(force_ksplit), t, k))
+    return [(t[i], k[i]) for i in range(HB_GEMM_COUNT)]
+
+
+def hb_layer_gemm_plans(layer: Layer) -> List[Tuple[int, int]]:
+    """(tile, ksplit) of each GEMM of the layer's most recent iteration."""
+    t, k = (C.c_int32 * HB_GEMM_COUNT)(), (C.c_int32 * HB_GEMM_COUNT)()
+    _check(load().hb_layer_gemm_plans(layer.handle, t, k))
+    return [(t[i], k[i]) for i in range(HB_GEMM_COUNT)]
 
 
 def hb_layer_stage(layer: Layer, stage: int) -> Tuple[int, int]:

@@ -113,6 +113,42 @@ def test_config_errors(H, field, value, status):
     assert _v(H, [(1, 0, bt(1))], shape=shape) == getattr(H, "HB_ERR_" + status)
 
 
+WINDOW = 0x7FFFFFF0  # bytes the GEMMs address in one operand
+
+
+def _llama(H, max_T, **kw):
+    """hb_validate_batch of a one-token batch under a Llama-shaped config."""
+    base = dict(hidden=8192, n_q_heads=64, n_kv_heads=8, head_dim=128, ffn_dim=28672, rope_theta=5e5, rms_eps=1e-5,
+                kv_block=16)
+    base.update(kw)
+    shape = type("S", (), base)
+    return _v(H, [(1, 0, bt(1))], shape=shape, max_T=max_T)
+
+
+def test_operand_window_limits(H):
+    """Every GEMM operand must fit the 2^31 - 16-byte buffer window: the
+    largest max_batch_tokens the 70B shape admits is the one whose SwiGLU
+    activations ((max_T + 512) x 28672 bf16) still fit; one more token is
+    rejected before any device work."""
+    F = 28672
+    limit = WINDOW // (2 * F) - 512
+    assert _llama(H, limit) == H.HB_OK
+    assert _llama(H, limit + 1) == H.HB_ERR_UNSUPPORTED
+    assert "window" in H.hb_last_error()
+    # the 8B shape: hidden 4096, ffn 14336
+    lim8 = WINDOW // (2 * 14336) - 512
+    assert _llama(H, lim8, hidden=4096, n_q_heads=32, ffn_dim=14336) == H.HB_OK
+    assert _llama(H, lim8 + 1, hidden=4096, n_q_heads=32, ffn_dim=14336) == H.HB_ERR_UNSUPPORTED
+    # weight matrices: gate/up (2F x H) and down (H x F) past the window
+    assert _llama(H, 16, hidden=16384, ffn_dim=53248) == H.HB_ERR_UNSUPPORTED
+    assert "w_gate_up" in H.hb_last_error()
+    assert _llama(H, 16, hidden=16384, ffn_dim=32768 + 16) == H.HB_ERR_UNSUPPORTED  # down: 16384 x F * 2 B
+    assert _llama(H, 16, hidden=16384, ffn_dim=32768 - 512) == H.HB_OK
+    # QKV weights: (nq + 2 nkv) hd x H
+    assert _llama(H, 16, hidden=16384, n_q_heads=512, n_kv_heads=32, ffn_dim=1024) == H.HB_ERR_UNSUPPORTED
+    assert "w_qkv" in H.hb_last_error()
+
+
 def test_gqa_group_must_divide_16(H):
     shape = type("S", (Shape,), {"n_q_heads": 32, "n_kv_heads": 1})
     assert _v(H, [(1, 0, bt(1))], shape=shape) == H.HB_ERR_UNSUPPORTED
@@ -142,6 +178,29 @@ def _create_model(H, n_layers=2, vocab=64, pool_blocks=(64, 64), null_embed=Fals
 def test_model_argument_errors(H, kw):
     assert _create_model(H, **kw) == H.HB_ERR_INVALID
     assert H.hb_last_error()
+
+
+def test_model_lm_head_window(H):
+    """The LM head (vocab x H bf16) is a GEMM operand: past the 2 GiB window
+    the model is rejected before any HIP call."""
+    vocab = (WINDOW // (2 * Shape.hidden) + 8) // 8 * 8
+    assert _create_model(H, vocab=vocab) == H.HB_ERR_UNSUPPORTED
+    assert "lm_head" in H.hb_last_error()
+
+
+def test_gemm_plans_host_only(H):
+    """The GEMM planner runs on the host: plans for the 8B shape are valid
+    tile indices and K splits, and every (tile, split) is a launch the
+    kernels implement."""
+    from hb_workloads import LLAMA3_8B
+    cfg = H.make_config(LLAMA3_8B, 4096, 512)
+    n = H.hb_gemm_tile_count()
+    assert n >= 1
+    for T in (1, 64, 128, 576, 2048, 4096):
+        for tile, ks in H.hb_plan_gemms(cfg, T, 256):
+            assert 0 <= tile < n and 1 <= ks <= 8
+    with pytest.raises(H.HBError):
+        H.hb_plan_gemms(cfg, 0, 256)
 
 
 def test_model_layer_of_null_model(H):

@@ -6,7 +6,7 @@ import pytest
 
 import oracle
 from hb_workloads import (TINY, LayerShape, f32_to_bf16_bits, make_batch, make_weights, tiny_batch)
-from hbref import assert_parity, assert_stage, errors, oracle_for_batch
+from hbref import assert_parity, assert_stage, assert_swiglu_stage, errors, oracle_for_batch
 
 pytestmark = pytest.mark.gpu
 
@@ -43,7 +43,8 @@ def test_tiny_parity_all_rows_and_stages(hb):
     b = tiny_batch()
     dl, w = _setup(hb, b)
     y = _run(dl, b)
-    ref, st = oracle_for_batch(b, oracle.weights_to_f64(w), stages=True)
+    w64 = oracle.weights_to_f64(w)
+    ref, st = oracle_for_batch(b, w64, stages=True)
     print("tiny y", errors(y, ref))
     assert_parity(y, ref)
     T = b.n_tokens
@@ -54,7 +55,7 @@ def test_tiny_parity_all_rows_and_stages(hb):
     h2 = dl.stage(H.HB_STAGE_H2, T).cpu().numpy()
     assert_parity(h2, st["h2"], "h2")
     m = oracle.bf16_bits_to_f64(bf16_bits(dl.stage(H.HB_STAGE_MLP, T)))
-    assert_stage(m, st["m"], "silu(gate)*up")
+    assert_swiglu_stage(m, st, w64, b.shape.rms_eps)
 
 
 SMALL_SHAPES = [
@@ -261,7 +262,8 @@ def test_every_gemm_tile_shape(hb, monkeypatch, tile, ksplit):
     b = make_batch(shape, lens, seed=31, num_blocks=64)
     dl, w = _setup(hb, b)
     y = _run(dl, b)
-    ref, st = oracle_for_batch(b, oracle.weights_to_f64(w), stages=True)
+    w64 = oracle.weights_to_f64(w)
+    ref, st = oracle_for_batch(b, w64, stages=True)
     print(f"tile {tile} ksplit {ksplit}", errors(y, ref))
     assert_parity(y, ref)
     T = b.n_tokens
@@ -270,7 +272,7 @@ def test_every_gemm_tile_shape(hb, monkeypatch, tile, ksplit):
     h2 = dl.stage(H.HB_STAGE_H2, T).cpu().numpy()
     assert_parity(h2, st["h2"], "h2")
     m = oracle.bf16_bits_to_f64(bf16_bits(dl.stage(H.HB_STAGE_MLP, T)))
-    assert_stage(m, st["m"], "silu(gate)*up")
+    assert_swiglu_stage(m, st, w64, b.shape.rms_eps)
 
 
 def test_back_to_back_iterations_match_one_at_a_time(hb):
