@@ -155,6 +155,22 @@ typedef struct {
  * not write the same slot. */
 hb_status hb_run_iteration(hb_layer* layer, const hb_batch_desc* desc);
 
+/* hb_run_iteration for callers that cannot allocate device memory during the
+ * call (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same kernels and launch plans, with the iteration's
+ * scratch -- its metadata, split-K partial sums and attention split partials
+ * -- in a fixed 64 MiB device array that the library holds on each GPU it
+ * runs on for the life of the process (looked up when a layer is created),
+ * and the metadata staged through pinned host memory the layer allocated at
+ * creation (1 MiB). The call allocates no device or pinned memory and
+ * records no timing events (hb_set_kernel_timing does not apply). Every call
+ * on one GPU shares that GPU's array: calls whose iterations overlap on one
+ * GPU (layers on different streams) race; calls on one stream are ordered.
+ * Errors: those of hb_run_iteration, and HB_ERR_UNSUPPORTED for a batch whose
+ * scratch exceeds 64 MiB or whose metadata exceeds 2^18 int32 (nothing is
+ * enqueued then). */
+hb_status hb_run_iteration_noalloc(hb_layer* layer, const hb_batch_desc* desc);
+
 /* Check a batch against a layer configuration and pool size without touching
  * any device (no HIP call). Errors: HB_ERR_INVALID (null pointer,
  * chunk_len < 1, context_len < 0, short block table, T > max_batch_tokens,

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -22,8 +23,20 @@ using namespace hb;
     if (e_ != hipSuccess) return fail(HB_ERR_HIP, "%s failed: %s", #call, hipGetErrorString(e_)); \
   } while (0)
 
+// Scratch of the allocation-free entry point (hb_run_iteration_noalloc):
+// metadata, split-K partials and attention split partials of one iteration.
+// Every GPU the library runs on holds its own copy for the life of the
+// process. In host code `scratch` names a host-side stand-in, never the
+// device memory: its device address comes from hipGetSymbolAddress, once per
+// device (scratch_address below), and only that address is passed on.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
 namespace {
 constexpr int kStages = 4;
+// Pinned host staging of the allocation-free entry point's metadata (int32).
+constexpr size_t kNoAllocMetaInts = (size_t)1 << 18;
+constexpr int kMaxDevices = 64;
 constexpr double kPeakHbm = 8.0e12;      // MI355X HBM3E, bytes/s
 constexpr double kPeakBf16 = 2.5e15;     // MI355X dense bf16 MFMA, flop/s
 
@@ -72,6 +85,12 @@ struct hb_layer {
   Plan plan;
   int last_T = 0;
   GemmPlan last_plans[HB_GEMM_COUNT] = {};  // of the most recent iteration
+  // allocation-free entry point: the device's scratch, pinned metadata
+  // staging and the event guarding its reuse
+  uint8_t* scratch = nullptr;
+  int32_t* na_host = nullptr;
+  hipEvent_t na_copied = nullptr;
+  bool na_pending = false;
   // timing
   uint32_t timing_mask = 0;  // bit k: bracket kernel k with events
   std::vector<hipEvent_t> ev_free;
@@ -82,6 +101,23 @@ struct hb_layer {
 
 namespace {
 
+// Device address of `scratch` on device `dev`, which must be current: looked
+// up once per device and kept.
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+hb_status scratch_address(int dev, uint8_t** out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(HB_ERR_UNSUPPORTED, "device %d beyond %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return fail(HB_ERR_HIP, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(e));
+    g_scratch_dev[dev] = p;
+  }
+  *out = static_cast<uint8_t*>(g_scratch_dev[dev]);
+  return HB_OK;
+}
 
 hb_status ensure_splitk(hb_layer* L, size_t floats) {
   if (floats <= L->splitk_cap) return HB_OK;
@@ -182,10 +218,10 @@ hb_status get_event(hb_layer* L, hipEvent_t* e) {
   return HB_OK;
 }
 
-// Launch wrapper: brackets the launch with events while timing is enabled.
+// Launch wrapper: brackets the launch with events when bit `kernel` of mask is set.
 template <typename F>
-hb_status timed(hb_layer* L, int kernel, F&& launch) {
-  if (!((L->timing_mask >> kernel) & 1u)) {
+hb_status timed(hb_layer* L, uint32_t mask, int kernel, F&& launch) {
+  if (!((mask >> kernel) & 1u)) {
     launch();
     return HB_OK;
   }
@@ -219,6 +255,8 @@ void free_layer(hb_layer* L) {
     if (s.consumed) (void)hipEventDestroy(s.consumed);
   }
   if (L->copy_stream) (void)hipStreamDestroy(L->copy_stream);
+  if (L->na_host) (void)hipHostFree(L->na_host);
+  if (L->na_copied) (void)hipEventDestroy(L->na_copied);
   for (const TimedLaunch& t : L->timed) {
     (void)hipEventDestroy(t.start);
     (void)hipEventDestroy(t.stop);
@@ -239,7 +277,10 @@ struct Prepared {
   GemmArgs gq, go, gu, gd;
   GemmPlan pq, po, pu, pd;
   const int32_t* meta = nullptr;
-  int slot = 0;
+  int slot = -1;             // metadata ring slot (-1: the metadata is not in the ring)
+  float* splitk = nullptr;   // split-K partials
+  float *part_o = nullptr, *part_ml = nullptr;  // attention split partials
+  uint32_t timing_mask = 0;  // kernels bracketed by events
 };
 
 // The four GEMMs of an iteration over T tokens: shapes, epilogues and (when
@@ -307,6 +348,10 @@ hb_status prepare_layer(hb_layer* L, const hb_batch_desc* desc, Prepared* pp) {
   if (st != HB_OK) return st;
   pp->gq = gq; pp->go = go; pp->gu = gu; pp->gd = gd;
   pp->pq = pq; pp->po = po; pp->pu = pu; pp->pd = pd;
+  pp->splitk = L->splitk;
+  pp->part_o = L->part_o;
+  pp->part_ml = L->part_ml;
+  pp->timing_mask = L->timing_mask;
   L->last_plans[HB_GEMM_QKV] = pq; L->last_plans[HB_GEMM_O] = po;
   L->last_plans[HB_GEMM_GATE_UP] = pu; L->last_plans[HB_GEMM_DOWN] = pd;
   return stage_upload(L, p.meta.data(), p.meta.size(), &pp->meta, &pp->slot);
@@ -318,8 +363,11 @@ hb_status launch_layer(hb_layer* L, const hb_batch_desc* desc, const Prepared& p
   struct Consumed {
     hb_layer* L;
     int slot;
-    ~Consumed() { (void)stage_consumed(L, slot); }
+    ~Consumed() {
+      if (slot >= 0) (void)stage_consumed(L, slot);
+    }
   } consumed{L, pp.slot};
+  const uint32_t tm = pp.timing_mask;
   const Dims& d = L->d;
   const Plan& p = L->plan;
   const int T = p.T;
@@ -334,12 +382,12 @@ hb_status launch_layer(hb_layer* L, const hb_batch_desc* desc, const Prepared& p
   rp.tok_pos = meta + p.off_tok_pos; rp.tok_req = meta + p.off_tok_req;
   rp.req_bt = meta + p.off_req_bt; rp.bt = meta + p.off_bt;
   rp.inv_freq = L->inv_freq; rp.hd = d.hd; rp.cs = L->rope_cs; rp.slot = L->tok_slot;
-  st = timed(L, HB_K_RMSNORM_ATTN, [&] {
+  st = timed(L, tm, HB_K_RMSNORM_ATTN, [&] {
     launch_rmsnorm(s, x_in, false, static_cast<const uint16_t*>(L->w.g_attn), L->xn, T, d.H, d.eps, &rp);
   });
   if (st != HB_OK) return st;
   // q, k rotated and k, v scattered into the pool by the epilogue
-  st = timed(L, HB_K_GEMM_QKV, [&] { launch_gemm(s, gq, pq, L->splitk); });
+  st = timed(L, tm, HB_K_GEMM_QKV, [&] { launch_gemm(s, gq, pq, pp.splitk); });
   if (st != HB_OK) return st;
 
   AttnArgs at{};
@@ -351,27 +399,27 @@ hb_status launch_layer(hb_layer* L, const hb_batch_desc* desc, const Prepared& p
   at.groups = meta + p.off_groups; at.n_groups = p.n_groups;
   at.merge_units = meta + p.off_merge; at.n_merge_units = p.n_merge_units;
   at.req_bt = rp.req_bt; at.bt = rp.bt;
-  at.part_o = L->part_o; at.part_ml = L->part_ml;
+  at.part_o = pp.part_o; at.part_ml = pp.part_ml;
   at.nq = d.nq; at.nkv = d.nkv; at.hd = d.hd;
   at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.hd));
-  st = timed(L, HB_K_ATTENTION, [&] { launch_attention(s, at); });
+  st = timed(L, tm, HB_K_ATTENTION, [&] { launch_attention(s, at); });
   if (st != HB_OK) return st;
   if (p.n_groups > 0) {
-    st = timed(L, HB_K_ATTN_MERGE, [&] { launch_attn_merge(s, at); });
+    st = timed(L, tm, HB_K_ATTN_MERGE, [&] { launch_attn_merge(s, at); });
     if (st != HB_OK) return st;
   }
   bool ffn_norm_done = false;
-  st = timed(L, HB_K_GEMM_O, [&] { ffn_norm_done = launch_gemm(s, go, po, L->splitk); });
+  st = timed(L, tm, HB_K_GEMM_O, [&] { ffn_norm_done = launch_gemm(s, go, po, pp.splitk); });
   if (st != HB_OK) return st;
   if (!ffn_norm_done) {
-    st = timed(L, HB_K_RMSNORM_FFN, [&] {
+    st = timed(L, tm, HB_K_RMSNORM_FFN, [&] {
       launch_rmsnorm(s, L->h2, true, static_cast<const uint16_t*>(L->w.g_ffn), L->xn, T, d.H, d.eps);
     });
     if (st != HB_OK) return st;
   }
-  st = timed(L, HB_K_GEMM_GATE_UP, [&] { launch_gemm(s, gu, pu, L->splitk); });
+  st = timed(L, tm, HB_K_GEMM_GATE_UP, [&] { launch_gemm(s, gu, pu, pp.splitk); });
   if (st != HB_OK) return st;
-  st = timed(L, HB_K_GEMM_DOWN, [&] { launch_gemm(s, gd, pd, L->splitk); });
+  st = timed(L, tm, HB_K_GEMM_DOWN, [&] { launch_gemm(s, gd, pd, pp.splitk); });
   if (st != HB_OK) return st;
   L->last_T = T;
   return check_hip("kernel launch");
@@ -525,6 +573,12 @@ hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w,
       return bail(fail(HB_ERR_HIP, "hipEventCreate failed"));
   st = ensure_parts(L, 1 << 16);
   if (st != HB_OK) return bail(st);
+  st = scratch_address(L->device, &L->scratch);
+  if (st != HB_OK) return bail(st);
+  if (hipHostMalloc((void**)&L->na_host, kNoAllocMetaInts * sizeof(int32_t), hipHostMallocDefault) != hipSuccess)
+    return bail(fail(HB_ERR_OOM, "pinned staging of %zu B", kNoAllocMetaInts * 4));
+  if (hipEventCreateWithFlags(&L->na_copied, hipEventDisableTiming) != hipSuccess)
+    return bail(fail(HB_ERR_HIP, "hipEventCreate failed"));
   *out = L;
   return HB_OK;
 }
@@ -564,6 +618,56 @@ hb_status hb_run_iteration(hb_layer* L, const hb_batch_desc* desc) {
   if (desc->n_requests == 0) return HB_OK;
   build_plan(L->d, desc, L->cu_count, &L->plan, L->plan_opt);
   return enqueue_layer(L, desc);
+}
+
+hb_status hb_run_iteration_noalloc(hb_layer* L, const hb_batch_desc* desc) {
+  if (!L) return fail(HB_ERR_INVALID, "null layer");
+  hb_status st = check_batch(L->d, L->pool.num_blocks, desc, &L->marks);
+  if (st != HB_OK) return st;
+  if (desc->n_requests == 0) return HB_OK;
+  const Dims& d = L->d;
+  build_plan(d, desc, L->cu_count, &L->plan, L->plan_opt);
+  const Plan& p = L->plan;
+  Prepared pp;
+  GemmArgs g[HB_GEMM_COUNT];
+  layer_gemms(d, p.T, L, desc, g);
+  GemmPlan pl[HB_GEMM_COUNT];
+  size_t splitk_floats = 0;
+  for (int i = 0; i < HB_GEMM_COUNT; ++i) {
+    pl[i] = plan_gemm(g[i], L->cu_count, L->gemm_tile, L->gemm_ksplit);
+    if (pl[i].ksplit > 1) splitk_floats = std::max(splitk_floats, (size_t)pl[i].ksplit * g[i].M * partial_width(g[i]));
+  }
+  // scratch layout: metadata | split-K partials | attention partials (o, then m and l)
+  auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  const size_t meta_bytes = p.meta.size() * sizeof(int32_t);
+  const size_t off_splitk = up(meta_bytes);
+  const size_t off_part_o = off_splitk + up(splitk_floats * sizeof(float));
+  const size_t off_part_ml = off_part_o + up((size_t)p.n_slots * d.hd * sizeof(float));
+  const size_t need = off_part_ml + up((size_t)p.n_slots * 2 * sizeof(float));
+  if (need > kScratchBytes || p.meta.size() > kNoAllocMetaInts)
+    return fail(HB_ERR_UNSUPPORTED,
+                "batch needs %zu B of scratch (%zu B of metadata), the allocation-free entry point has %zu B "
+                "(%zu B of metadata staging); use hb_run_iteration",
+                need, meta_bytes, kScratchBytes, kNoAllocMetaInts * sizeof(int32_t));
+  // the pinned staging is reused once the previous copy out of it is done
+  if (L->na_pending) {
+    HB_HIP(hipEventSynchronize(L->na_copied));
+    L->na_pending = false;
+  }
+  std::memcpy(L->na_host, p.meta.data(), meta_bytes);
+  HB_HIP(hipMemcpyAsync(L->scratch, L->na_host, meta_bytes, hipMemcpyHostToDevice, L->stream));
+  HB_HIP(hipEventRecord(L->na_copied, L->stream));
+  L->na_pending = true;
+  pp.gq = g[HB_GEMM_QKV]; pp.go = g[HB_GEMM_O]; pp.gu = g[HB_GEMM_GATE_UP]; pp.gd = g[HB_GEMM_DOWN];
+  pp.pq = pl[HB_GEMM_QKV]; pp.po = pl[HB_GEMM_O]; pp.pu = pl[HB_GEMM_GATE_UP]; pp.pd = pl[HB_GEMM_DOWN];
+  pp.meta = reinterpret_cast<const int32_t*>(L->scratch);
+  pp.slot = -1;
+  pp.splitk = reinterpret_cast<float*>(L->scratch + off_splitk);
+  pp.part_o = reinterpret_cast<float*>(L->scratch + off_part_o);
+  pp.part_ml = reinterpret_cast<float*>(L->scratch + off_part_ml);
+  pp.timing_mask = 0;  // no events: creating them may allocate
+  for (int i = 0; i < HB_GEMM_COUNT; ++i) L->last_plans[i] = pl[i];
+  return launch_layer(L, desc, pp);
 }
 
 hb_status hb_set_kernel_timing(hb_layer* L, uint32_t mask) {

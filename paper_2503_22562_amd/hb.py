@@ -25,7 +25,7 @@ EXPORTED = ("hb_create_layer", "hb_destroy_layer", "hb_append_kv", "hb_run_itera
             "hb_profile", "hb_profile_batches", "hb_latency_features", "hb_fit_latency_model", "hb_predict_latency", "hb_select_chunk",
             "hb_create_model", "hb_destroy_model", "hb_model_layer", "hb_run_model",
             "hb_set_kernel_timing", "hb_kernel_times", "hb_kernel_name", "hb_layer_stage", "hb_last_error",
-            "hb_gemm_tile_count", "hb_plan_gemms", "hb_layer_gemm_plans")
+            "hb_gemm_tile_count", "hb_plan_gemms", "hb_layer_gemm_plans", "hb_run_iteration_noalloc")
 HB_LAT_FEATURES = 5
 
 
@@ -109,6 +109,8 @@ def load() -> C.CDLL:
     lib.hb_append_kv.restype = st
     lib.hb_run_iteration.argtypes = [C.c_void_p, C.POINTER(hb_batch_desc)]
     lib.hb_run_iteration.restype = st
+    lib.hb_run_iteration_noalloc.argtypes = [C.c_void_p, C.POINTER(hb_batch_desc)]
+    lib.hb_run_iteration_noalloc.restype = st
     lib.hb_validate_batch.argtypes = [C.POINTER(hb_layer_config), C.c_int32, C.POINTER(hb_batch_desc)]
     lib.hb_validate_batch.restype = st
     lib.hb_profile.argtypes = [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.POINTER(hb_decode_mix), C.c_int32,
@@ -327,6 +329,16 @@ def hb_run_iteration(layer: Layer, requests: Sequence[Tuple[int, int, Iterable[i
         out_dtype = HB_OUT_F32 if x_out.dtype == torch.float32 else HB_OUT_BF16
     d, keep = _desc(requests, _ptr(x_in), _ptr(x_out), out_dtype)
     _check(load().hb_run_iteration(layer.handle, C.byref(d)))
+
+
+def hb_run_iteration_noalloc(layer: Layer, requests: Sequence[Tuple[int, int, Iterable[int]]], x_in, x_out,
+                             out_dtype: Optional[int] = None) -> None:
+    """As hb_run_iteration, through the allocation-free entry point."""
+    if out_dtype is None:
+        import torch
+        out_dtype = HB_OUT_F32 if x_out.dtype == torch.float32 else HB_OUT_BF16
+    d, keep = _desc(requests, _ptr(x_in), _ptr(x_out), out_dtype)
+    _check(load().hb_run_iteration_noalloc(layer.handle, C.byref(d)))
 
 
 def hb_validate_batch(cfg: hb_layer_config, num_blocks: int, requests, x_in_ptr: int, x_out_ptr: int,
