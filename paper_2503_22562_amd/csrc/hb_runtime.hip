@@ -89,6 +89,9 @@ struct hb_layer {
   // staging and the event guarding its reuse
   uint8_t* scratch = nullptr;
   int32_t* na_host = nullptr;
+  // device bytes the layer holds, and the most it may hold (HB_DEVICE_ALLOC_LIMIT
+  // at creation, testing: makes the out-of-memory paths reachable on demand)
+  size_t dev_bytes = 0, dev_limit = SIZE_MAX;
   hipEvent_t na_copied = nullptr;
   bool na_pending = false;
   // timing
@@ -119,13 +122,31 @@ hb_status scratch_address(int dev, uint8_t** out) {
   return HB_OK;
 }
 
+// hipMalloc for the layer's own buffers, within its device-memory limit.
+bool dev_alloc(hb_layer* L, void** p, size_t bytes) {
+  *p = nullptr;
+  if (bytes > L->dev_limit - std::min(L->dev_limit, L->dev_bytes)) return false;
+  if (hipMalloc(p, bytes) != hipSuccess) {
+    *p = nullptr;
+    return false;
+  }
+  L->dev_bytes += bytes;
+  return true;
+}
+
+void dev_free(hb_layer* L, void* p, size_t bytes) {
+  if (!p) return;
+  (void)hipFree(p);
+  L->dev_bytes -= std::min(L->dev_bytes, bytes);
+}
+
 hb_status ensure_splitk(hb_layer* L, size_t floats) {
   if (floats <= L->splitk_cap) return HB_OK;
   HB_HIP(hipStreamSynchronize(L->stream));
-  if (L->splitk) HB_HIP(hipFree(L->splitk));
+  dev_free(L, L->splitk, L->splitk_cap * sizeof(float));
   L->splitk = nullptr;
   L->splitk_cap = 0;
-  if (hipMalloc(&L->splitk, floats * sizeof(float)) != hipSuccess)
+  if (!dev_alloc(L, (void**)&L->splitk, floats * sizeof(float)))
     return fail(HB_ERR_OOM, "split-K workspace of %zu B", floats * 4);
   L->splitk_cap = floats;
   return HB_OK;
@@ -136,12 +157,12 @@ hb_status ensure_parts(hb_layer* L, int n) {
   if (n <= L->part_cap) return HB_OK;
   int cap = std::max(n, L->part_cap * 2);
   HB_HIP(hipStreamSynchronize(L->stream));
-  if (L->part_o) HB_HIP(hipFree(L->part_o));
-  if (L->part_ml) HB_HIP(hipFree(L->part_ml));
+  dev_free(L, L->part_o, (size_t)L->part_cap * L->d.hd * sizeof(float));
+  dev_free(L, L->part_ml, (size_t)L->part_cap * 2 * sizeof(float));
   L->part_o = L->part_ml = nullptr;
   L->part_cap = 0;
-  if (hipMalloc(&L->part_o, (size_t)cap * L->d.hd * sizeof(float)) != hipSuccess ||
-      hipMalloc(&L->part_ml, (size_t)cap * 2 * sizeof(float)) != hipSuccess)
+  if (!dev_alloc(L, (void**)&L->part_o, (size_t)cap * L->d.hd * sizeof(float)) ||
+      !dev_alloc(L, (void**)&L->part_ml, (size_t)cap * 2 * sizeof(float)))
     return fail(HB_ERR_OOM, "attention split buffers for %d column slots", cap);
   L->part_cap = cap;
   return HB_OK;
@@ -169,11 +190,11 @@ hb_status stage_upload(hb_layer* L, const int32_t* src, size_t n, const int32_t*
   }
   if (n > s.dev_cap) {
     HB_HIP(hipEventSynchronize(s.consumed));  // no kernel reads the old copy any more
-    if (s.dev) HB_HIP(hipFree(s.dev));
+    dev_free(L, s.dev, s.dev_cap * sizeof(int32_t));
     s.dev = nullptr;
     s.dev_cap = 0;
     size_t cap = std::max<size_t>(n, 1 << 16);
-    if (hipMalloc(&s.dev, cap * sizeof(int32_t)) != hipSuccess)
+    if (!dev_alloc(L, (void**)&s.dev, cap * sizeof(int32_t)))
       return fail(HB_ERR_OOM, "metadata buffer of %zu B", cap * 4);
     s.dev_cap = cap;
   }
@@ -550,6 +571,7 @@ hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w,
   if (const char* e = std::getenv("HB_ATTN_SPLIT_TILE")) L->plan_opt.split_tile = std::atoi(e);
   if (const char* e = std::getenv("HB_ATTN_SPLIT_ITEM")) L->plan_opt.split_item = std::atoi(e);
   if (const char* e = std::getenv("HB_ATTN_UNIT_BLOCK")) L->plan_opt.unit_block = std::atoi(e);
+  if (const char* e = std::getenv("HB_DEVICE_ALLOC_LIMIT")) L->dev_limit = std::strtoull(e, nullptr, 10);
   const size_t T = d.max_T;
   const size_t TA = T + kGemmPadRows;  // GEMM A operands: rows past M stay readable
   struct Alloc { void** p; size_t bytes; } allocs[] = {
@@ -560,7 +582,7 @@ hb_status hb_create_layer(const hb_layer_config* cfg, const hb_layer_weights* w,
       {(void**)&L->inv_freq, (size_t)d.hd / 2 * sizeof(double)},
   };
   for (auto& a : allocs)
-    if (hipMalloc(a.p, a.bytes) != hipSuccess) return bail(fail(HB_ERR_OOM, "workspace allocation of %zu B", a.bytes));
+    if (!dev_alloc(L, a.p, a.bytes)) return bail(fail(HB_ERR_OOM, "workspace allocation of %zu B", a.bytes));
   std::vector<double> inv(d.hd / 2);
   for (int j = 0; j < d.hd / 2; ++j) inv[j] = std::pow((double)d.theta, -2.0 * j / d.hd);
   if (hipMemcpy(L->inv_freq, inv.data(), inv.size() * sizeof(double), hipMemcpyHostToDevice) != hipSuccess)

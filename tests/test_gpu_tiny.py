@@ -318,3 +318,62 @@ def test_back_to_back_iterations_match_one_at_a_time(hb):
         ref = y.cpu().numpy()
         assert np.all(np.isfinite(ref)), f"batch {i}"
         assert np.array_equal(got[i].view(np.uint32), ref.view(np.uint32)), f"batch {i} differs when enqueued back to back"
+
+
+def test_out_of_memory_is_reported_and_recoverable(hb, monkeypatch):
+    """Device allocation failures, forced by a per-layer limit on the
+    library's own device memory (HB_DEVICE_ALLOC_LIMIT, read at creation):
+    creation fails with HB_ERR_OOM and leaves nothing behind; an iteration
+    whose split-K partials do not fit fails with HB_ERR_OOM before anything is
+    enqueued (pool and output untouched), and the layer then runs a batch
+    that fits, matching the oracle."""
+    import torch
+    from gemmcover import COVER
+    from paper_2503_22562_amd import hb as H
+    from paper_2503_22562_amd.harness import DeviceLayer, bf16_bits, to_device_bf16
+    w = make_weights(COVER)
+    big = make_batch(COVER, [(2048, 0)], seed=71, num_blocks=256)
+    monkeypatch.setenv("HB_DEVICE_ALLOC_LIMIT", "1000000")
+    with pytest.raises(H.HBError) as e:
+        DeviceLayer(COVER, w, big.num_blocks, big.n_tokens, 4)
+    assert e.value.status == H.HB_ERR_OOM
+    # workspace of about 100 MB fits, 8-way split-K partials of a 2048-token
+    # batch (8 x 2048 x 5120 fp32 = 335 MB) do not
+    monkeypatch.setenv("HB_DEVICE_ALLOC_LIMIT", str(200 << 20))
+    monkeypatch.setenv("HB_GEMM_KSPLIT", "8")
+    dl = DeviceLayer(COVER, w, big.num_blocks, big.n_tokens, 4)
+    k0, v0 = bf16_bits(dl.k_pool), bf16_bits(dl.v_pool)
+    x = to_device_bf16(big.x_in())
+    y = torch.full((big.n_tokens, COVER.hidden), 7.0, dtype=torch.float32, device="cuda")
+    with pytest.raises(H.HBError) as e:
+        H.hb_run_iteration(dl.layer, _reqs(big), x, y)
+    assert e.value.status == H.HB_ERR_OOM
+    torch.cuda.synchronize()
+    assert np.array_equal(bf16_bits(dl.k_pool), k0) and np.array_equal(bf16_bits(dl.v_pool), v0)
+    assert torch.all(y == 7.0)
+    small = make_batch(COVER, [(48, 20), (1, 100), (1, 0)], seed=72, num_blocks=256)
+    for r, req in enumerate(small.requests):
+        if req.context_len:
+            k, v = small.prior_kv(r)
+            dl.append_kv(req.block_table, 0, k, v)
+    got = _run(dl, small)
+    assert any(ks == 8 for _, ks in H.hb_layer_gemm_plans(dl.layer))
+    assert_parity(got, oracle_for_batch(small, oracle.weights_to_f64(w)))
+
+
+def test_profile_rejects_cells_beyond_the_pool(hb):
+    """hb_profile validates every cell before touching the device: a cell
+    that needs more blocks than the pool holds, or more tokens than the
+    layer's capacity, is HB_ERR_INVALID and nothing runs."""
+    from paper_2503_22562_amd import hb as H
+    b = tiny_batch()
+    dl, _ = _setup(hb, b)
+    k0, v0 = _pool_bits(dl)
+    with pytest.raises(H.HBError) as e:  # 256 blocks of 16: a 5000-token context does not fit
+        H.hb_profile(dl.layer, [16], [([5000], 0)], warmup=0, iters=1)
+    assert e.value.status == H.HB_ERR_INVALID
+    with pytest.raises(H.HBError) as e:  # above max_batch_tokens
+        H.hb_profile(dl.layer, [b.n_tokens + 1], [([], 0)], warmup=0, iters=1)
+    assert e.value.status == H.HB_ERR_INVALID
+    k1, v1 = _pool_bits(dl)
+    assert np.array_equal(k0, k1) and np.array_equal(v0, v1)
