@@ -252,9 +252,9 @@ def counters_cell(cell, steps, warmup):
     """Only the layer iterations of one gate cell, for counter passes
     (rocprofv3 --pmc): 'C,D' = the 8B sweep cell with a C-token chunk and D
     decodes, '70b' = the 70B layer's chunk 2048 at 30720 + 32 decodes,
-    'multi' = the 8B 4-chunk + 256-decode batch."""
+    'multi' = the 8B 4-chunk + 256-decode batch, '8b' = the bench batch."""
     import torch
-    from hb_workloads import LLAMA3_8B, LLAMA3_70B, llama70b_batch, multi_batch, sweep_batch
+    from hb_workloads import LLAMA3_8B, LLAMA3_70B, llama70b_batch, llama8b_batch, multi_batch, sweep_batch
     from paper_2503_22562_amd import hb
     from paper_2503_22562_amd.harness import to_device_bf16
     torch.cuda.set_device(0)
@@ -262,6 +262,8 @@ def counters_cell(cell, steps, warmup):
         shape, b = LLAMA3_70B, llama70b_batch()
     elif cell == "multi":
         shape, b = LLAMA3_8B, multi_batch()
+    elif cell == "8b":
+        shape, b = LLAMA3_8B, llama8b_batch()
     else:
         c, d = (int(v) for v in cell.split(","))
         shape, b = LLAMA3_8B, sweep_batch(c, d)
@@ -530,7 +532,7 @@ def main() -> int:
     ap.add_argument("--no-regimes", action="store_true")
     ap.add_argument("--no-model", action="store_true", help="skip the 32-layer whole-model iteration")
     ap.add_argument("--counters-cell", default=None,
-                    help="only run one cell ('C,D', '70b' or 'multi') --warmup + --steps times (counter passes) and exit")
+                    help="only run one cell ('C,D', '70b', 'multi' or '8b') --warmup + --steps times (counter passes) and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration) and exit")
     ap.add_argument("--cpu-baselines", action="store_true",
