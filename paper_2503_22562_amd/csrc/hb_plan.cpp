@@ -202,28 +202,65 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p,
   p->split_tile = S_t;
   p->split_item = S_i;
 
-  std::vector<AttnItem> tiles, items;
+  // Tiles: one work unit per (request, kv head, position block, key split).
+  // Items: a (request, kv head, position group) whose keys fit one split
+  // length is one wave item, packed four to a unit with items of similar
+  // length. A longer range is cut over k = ceil(n / 4) workgroups of four
+  // waves (n = its split count); each workgroup's four waves take
+  // consecutive sub-ranges and combine them in LDS, so only ranges that need
+  // more than one workgroup leave partial results for the merge kernel.
+  std::vector<AttnItem> tiles, singles;
+  struct Unit {
+    int64_t len;     // keys of the unit's longest wave
+    int first;       // first item (merged) or first single
+    bool merged;
+  };
+  std::vector<AttnItem> merged_items;
+  std::vector<Unit> merged_units;
   std::vector<MergeGroup> groups;
   int slots = 0;
   for (int r = 0; r < R; ++r) {
     const int c = rq[r].chunk_len, x = rq[r].context_len;
     const bool tile = is_tile(r);
-    const int w = tile ? d.BQ : d.P, S = tile ? S_t : S_i, ncol = tile ? kTileCols : 16;
-    std::vector<AttnItem>& out = tile ? tiles : items;
+    const int w = tile ? d.BQ : d.P, S = tile ? S_t : S_i;
     for (int g = 0; g < d.nkv; ++g) {
       for (int i0 = 0; i0 < c; i0 += w) {
         const int npos = std::min(w, c - i0);
         const int kv_len = x + i0 + npos;
         const int nspl = (kv_len + S - 1) / S;
-        int part0 = -1;
-        if (nspl > 1) {
-          part0 = slots;
-          groups.push_back({slots, nspl, ncol, tok_start[r] + i0, npos, g, 0, 0});
-          slots += nspl * ncol;
+        if (tile) {
+          int part0 = -1;
+          if (nspl > 1) {
+            part0 = slots;
+            groups.push_back({slots, nspl, kTileCols, tok_start[r] + i0, npos, g, 0, 0});
+            slots += nspl * kTileCols;
+          }
+          for (int s = 0; s < nspl; ++s)
+            tiles.push_back({r, g, tok_start[r] + i0, x + i0, npos, s * S, std::min(kv_len, (s + 1) * S),
+                             nspl > 1 ? part0 + s * kTileCols : -1});
+          continue;
         }
-        for (int s = 0; s < nspl; ++s)
-          out.push_back({r, g, tok_start[r] + i0, x + i0, npos, s * S, std::min(kv_len, (s + 1) * S),
-                         nspl > 1 ? part0 + s * ncol : -1});
+        if (nspl == 1) {
+          singles.push_back({r, g, tok_start[r] + i0, x + i0, npos, 0, kv_len, -1});
+          continue;
+        }
+        const int k = (nspl + kItemsPerUnit - 1) / kItemsPerUnit;
+        const int wlen = round_up((kv_len + k - 1) / k, 64);
+        int part0 = -1;
+        if (k > 1) {
+          part0 = slots;
+          groups.push_back({slots, k, 16, tok_start[r] + i0, npos, g, 0, 0});
+          slots += 16 * k;
+        }
+        for (int j = 0; j < k; ++j) {
+          const int b = j * wlen, e = std::min(kv_len, b + wlen);
+          const int plen = round_up((e - b + kItemsPerUnit - 1) / kItemsPerUnit, 64);
+          merged_units.push_back({plen, (int)merged_items.size(), true});
+          for (int q = 0; q < kItemsPerUnit; ++q) {
+            const int pb = std::min(e, b + q * plen), pe = std::min(e, pb + plen);
+            merged_items.push_back({r, g, tok_start[r] + i0, x + i0, npos, pb, pe, k > 1 ? part0 + 16 * j : -1});
+          }
+        }
       }
     }
   }
@@ -233,26 +270,47 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p,
     return (x.kv_end - x.kv_begin) * (int64_t)x.npos > (y.kv_end - y.kv_begin) * (int64_t)y.npos;
   };
   std::stable_sort(tiles.begin(), tiles.end(), longer);
-  std::stable_sort(items.begin(), items.end(), [](const AttnItem& x, const AttnItem& y) {
+  std::stable_sort(singles.begin(), singles.end(), [](const AttnItem& x, const AttnItem& y) {
     return (x.kv_end - x.kv_begin) > (y.kv_end - y.kv_begin);
   });
-  // work units: one per tile, one per kItemsPerUnit items, in alternating
-  // runs of one unit per CU: workgroups are handed out round-robin over the
-  // CUs, two per CU, so a CU's first two workgroups are a compute-bound tile
-  // and a bandwidth-bound item group, which overlap well
-  const int nt = (int)tiles.size(), ni_units = ((int)items.size() + kItemsPerUnit - 1) / kItemsPerUnit;
+  std::vector<Unit> item_units = merged_units;
+  for (int i = 0; i < (int)singles.size(); i += kItemsPerUnit)
+    item_units.push_back({singles[i].kv_end - singles[i].kv_begin, i, false});
+  std::stable_sort(item_units.begin(), item_units.end(), [](const Unit& x, const Unit& y) { return x.len > y.len; });
+  // items in unit order: unit v's items are 4 v .. 4 v + 3 (the last unit of
+  // singles is padded with empty items)
+  std::vector<AttnItem> items;
+  std::vector<int32_t> item_unit_codes;
+  items.reserve(merged_items.size() + singles.size() + kItemsPerUnit);
+  for (const Unit& u : item_units) {
+    const int v = (int)(items.size() / kItemsPerUnit);
+    item_unit_codes.push_back(-1 - (u.merged ? (v | kUnitMerged) : v));
+    const std::vector<AttnItem>& src = u.merged ? merged_items : singles;
+    const int n = std::min<int>(kItemsPerUnit, (int)src.size() - u.first);
+    for (int q = 0; q < n; ++q) items.push_back(src[u.first + q]);
+    for (int q = n; q < kItemsPerUnit; ++q) {
+      AttnItem e = src[u.first];
+      e.kv_begin = e.kv_end;  // empty: the wave does nothing
+      items.push_back(e);
+    }
+  }
+  // work units: one per tile, one per item unit, in alternating runs of one
+  // unit per CU: workgroups are handed out round-robin over the CUs, two per
+  // CU, so a CU's first two workgroups are a compute-bound tile and a
+  // bandwidth-bound item unit, which overlap well
+  const int nt = (int)tiles.size(), ni_units = (int)item_unit_codes.size();
   std::vector<int32_t> units;
   units.reserve(nt + ni_units);
   const int run = opt.unit_block != 0 ? opt.unit_block : cus;
   if (run > 0) {
     for (int a = 0, b = 0; a < nt || b < ni_units;) {
       for (int k = 0; k < run && a < nt; ++k) units.push_back(a++);
-      for (int k = 0; k < run && b < ni_units; ++k) units.push_back(-1 - b++);
+      for (int k = 0; k < run && b < ni_units; ++k) units.push_back(item_unit_codes[b++]);
     }
   } else {
     for (int a = 0, b = 0; a < nt || b < ni_units;) {
       if (b >= ni_units || (a < nt && (int64_t)a * ni_units <= (int64_t)b * nt)) units.push_back(a++);
-      else units.push_back(-1 - b++);
+      else units.push_back(item_unit_codes[b++]);
     }
   }
   p->n_tiles = nt;

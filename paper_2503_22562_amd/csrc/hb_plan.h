@@ -62,6 +62,13 @@ constexpr int kBtPad = 3;
 // a workgroup (one per wave): the attention workgroup has 4 waves.
 constexpr int kTileCols = 128;
 constexpr int kItemsPerUnit = 4;
+// Work unit encoding: u >= 0 is tile u; -1 - v runs items 4 w .. 4 w + 3 with
+// w = v & ~kUnitMerged, one per wave. Without kUnitMerged the four items are
+// independent. With it they are consecutive key ranges of one (request, kv
+// head, query positions), possibly empty (kv_begin == kv_end): the workgroup
+// combines them in LDS and writes one result, to the output when item 4 w's
+// part is < 0, else to that part's column slots.
+constexpr int32_t kUnitMerged = 1 << 29;
 
 struct Plan {
   int T = 0, R = 0;

@@ -23,9 +23,11 @@
 //  * wave items: 16 columns (decodes, short chunks) per wave, four per
 //    workgroup; each wave streams its K/V straight into registers, the next
 //    32-key step loading while the current one is multiplied. HBM-bound.
+//    A long item range is cut into four consecutive sub-ranges, one per wave
+//    of a workgroup, which combines them in LDS at the end.
 // The planner interleaves the two kinds so compute- and bandwidth-bound
-// workgroups run side by side. Key ranges longer than the split length are
-// divided over several work units; a merge kernel combines their partial
+// workgroups run side by side. Key ranges longer than one work unit takes
+// are divided over several units; a merge kernel combines their partial
 // results with the log-sum-exp rule.
 #include <algorithm>
 
@@ -228,8 +230,12 @@ __device__ __forceinline__ void wave_compute(const WaveStep<HD>& st, int j0, con
   }
 }
 
+// One wave item's 16 columns over its key range: the unnormalised O^T, the
+// running maximum m and the weight sum l of the lane's column (l summed over
+// the column's four lanes; m is the same on all four).
 template <int HD>
-__device__ __forceinline__ void wave_item(const AttnArgs& a, const AttnItem& it, int lane) {
+__device__ __forceinline__ void wave_run(const AttnArgs& a, const AttnItem& it, int lane, f32x4 (&o)[HD / 16],
+                                         float& m, float& l) {
   const int G = a.nq / a.nkv;
   const int col = lane & 15, grp = lane >> 4;
   const int pi = col / G;
@@ -245,10 +251,10 @@ __device__ __forceinline__ void wave_item(const AttnArgs& a, const AttnItem& it,
   }
   const int32_t* btab = a.bt + const_load(a.req_bt + it.req);
   const int kb_last = (it.kv_end - 1) >> 4;
-  f32x4 o[HD / 16];
 #pragma unroll
   for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m = NEG_BIG, l = 0.f;
+  m = NEG_BIG;
+  l = 0.f;
   const int nsteps = (it.kv_end - it.kv_begin + WSTEP - 1) / WSTEP;
   // the table is padded with copies of its last id (kBtPad), so the two ids
   // of a step are one 8-byte read; steps past the end re-read the last block
@@ -285,7 +291,93 @@ __device__ __forceinline__ void wave_item(const AttnArgs& a, const AttnItem& it,
     wave_compute(A, it.kv_begin + WSTEP * s, it, pos, grp, a.scale_log2, qf, o, m, l);
   }
   l = rows_sum(l);
-  store_column<HD>(a, it, col, o, m, l, grp);
+}
+
+template <int HD>
+__device__ __forceinline__ void wave_item(const AttnArgs& a, const AttnItem& it, int lane) {
+  f32x4 o[HD / 16];
+  float m, l;
+  wave_run<HD>(a, it, lane, o, m, l);
+  store_column<HD>(a, it, lane & 15, o, m, l, lane >> 4);
+}
+
+// A merged unit: its four items are consecutive key ranges of one (request,
+// kv head, positions), one per wave (an empty range contributes nothing).
+// The waves' results are combined in LDS with the log-sum-exp rule: with
+// M = max_w m_w, O = sum_w O_w 2^(m_w - M) and l = sum_w l_w 2^(m_w - M).
+// Wave w then finishes dimension tiles w DT/4 .. (w + 1) DT/4 - 1 of every
+// column and writes them, normalised, or as a partial result (O, M, l).
+template <int HD>
+__device__ __forceinline__ void merged_unit(const AttnArgs& a, int v, uint8_t* smem) {
+  constexpr int DT = HD / 16, PER = DT / WAVES;
+  static_assert(PER * WAVES == DT, "dimension tiles per wave");
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int col = lane & 15, grp = lane >> 4;
+  const AttnItem it = const_load(reinterpret_cast<const AttnItem*>(a.items) + WAVES * v + wave);
+  f32x4 o[DT];
+  float m = NEG_BIG, l = 0.f;
+  if (it.kv_begin < it.kv_end) {
+    wave_run<HD>(a, it, lane, o, m, l);
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  float* ml = reinterpret_cast<float*>(smem);                       // [wave][column] (m, l)
+  f32x4* os = reinterpret_cast<f32x4*>(smem + WAVES * 16 * 2 * 4);  // [wave][dt][lane]
+  if (grp == 0) {
+    ml[(wave * 16 + col) * 2 + 0] = m;
+    ml[(wave * 16 + col) * 2 + 1] = l;
+  }
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) os[(wave * DT + dt) * 64 + lane] = o[dt];
+  __syncthreads();
+  float mw[WAVES], M = NEG_BIG;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    mw[w] = ml[(w * 16 + col) * 2];
+    M = fmaxf(M, mw[w]);
+  }
+  float L = 0.f;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    mw[w] = exp2f(mw[w] - M);  // 0 for ranges with no key of this column
+    L += ml[(w * 16 + col) * 2 + 1] * mw[w];
+  }
+  f32x4 r[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    r[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) r[i] += os[(w * DT + wave * PER + i) * 64 + lane] * mw[w];
+  }
+  const int G = a.nq / a.nkv;
+  const int pi = col / G;
+  if (pi >= it.npos) return;  // column past the unit's last position
+  if (it.part < 0) {
+    const int h = it.kv_head * G + (col - pi * G);
+    const float inv = 1.0f / L;
+    uint16_t* orow = a.o + (size_t)(it.tok0 + pi) * a.nq * HD + h * HD + 4 * grp;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int dt = wave * PER + i;
+      u32x2 w = {pack_bf16x2(r[i][0] * inv, r[i][1] * inv), pack_bf16x2(r[i][2] * inv, r[i][3] * inv)};
+      st8(orow + 16 * dt, w);
+    }
+  } else {
+    const size_t slot = (size_t)it.part + col;
+    float* po = a.part_o + slot * HD + 4 * grp;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int dt = wave * PER + i;
+      u32x4 w = {__float_as_uint(r[i][0]), __float_as_uint(r[i][1]), __float_as_uint(r[i][2]),
+                 __float_as_uint(r[i][3])};
+      st16(po + 16 * dt, w);
+    }
+    if (grp == 0 && wave == 0) {
+      a.part_ml[slot * 2 + 0] = M;
+      a.part_ml[slot * 2 + 1] = L;
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -580,10 +672,14 @@ __global__ __launch_bounds__(64 * WAVES, 2) void attn_kernel(AttnArgs a) {
   const int unit = const_load(a.units + blockIdx.x);
   if (unit >= 0) {
     tile_unit<HD>(a, const_load(reinterpret_cast<const AttnItem*>(a.tiles) + unit), smem);
+  } else if ((-unit - 1) & kUnitMerged) {
+    merged_unit<HD>(a, (-unit - 1) & ~kUnitMerged, smem);
   } else {
     const int idx = (-unit - 1) * WAVES + wave_id();
-    if (idx < a.n_items)
-      wave_item<HD>(a, const_load(reinterpret_cast<const AttnItem*>(a.items) + idx), threadIdx.x & 63);
+    if (idx < a.n_items) {
+      const AttnItem it = const_load(reinterpret_cast<const AttnItem*>(a.items) + idx);
+      if (it.kv_begin < it.kv_end) wave_item<HD>(a, it, threadIdx.x & 63);
+    }
   }
 }
 

@@ -50,19 +50,42 @@ def check(plan, shape, reqs):
     for t, (pos, r) in enumerate(toks):
         assert r == tok_req[t] and pos == reqs[r][1] + t - starts[r]
     assert all(o[0] % 16 == 0 for o in plan["off"])
+    # units: each tile once, each group of per_unit items once; a merged unit's
+    # items are consecutive key ranges (some possibly empty) of one (request,
+    # kv head, positions) with one destination, and it yields one result
+    tile_cols, per_unit = plan["geom"][0]
+    MERGED = 1 << 29
+    units = [u[0] for u in plan["unit"]]
+    tiles = sorted(u for u in units if u >= 0)
+    item_units = sorted((-1 - u) & ~MERGED for u in units if u < 0)
+    assert tiles == list(range(len(plan["tile"])))
+    assert len(plan["item"]) % per_unit == 0
+    assert item_units == list(range(len(plan["item"]) // per_unit))
+    merged = {(-1 - u) & ~MERGED for u in units if u < 0 and (-1 - u) & MERGED}
+    results = [("tile", tile_cols, it) for it in plan["tile"]]
+    for v in range(len(plan["item"]) // per_unit):
+        its = plan["item"][per_unit * v:per_unit * (v + 1)]
+        if v in merged:
+            assert len({tuple(it[:5]) + (it[7],) for it in its}) == 1, "merged unit mixes columns or destinations"
+            full = [it for it in its if it[5] < it[6]]
+            assert full and all(x[6] == y[5] for x, y in zip(full, full[1:])), "merged ranges not consecutive"
+            assert all(it[5] % 64 == 0 for it in full)
+            assert all(it[5] == it[6] for it in its[len(full):]), "empty ranges must come last"
+            req, g, tok0, pos0, npos, _, _, part = its[0]
+            results.append(("item", 16, [req, g, tok0, pos0, npos, full[0][5], full[-1][6], part]))
+        else:
+            results += [("item", 16, it) for it in its if it[5] < it[6]]
     # coverage: (token, kv head) -> list of key ranges
     cover = defaultdict(list)
     slots = []
-    tile_cols, per_unit = plan["geom"][0]
-    for kind, width in (("tile", tile_cols), ("item", 16)):
-        for req, g, tok0, pos0, npos, kb, ke, part in plan[kind]:
-            assert kb % 64 == 0 and kb < ke and npos * G <= width
-            assert tok0 == starts[req] + pos0 - reqs[req][1]
-            assert ke <= pos0 + npos and ke <= reqs[req][0] + reqs[req][1]
-            for i in range(npos):
-                cover[(tok0 + i, g)].append((kb, ke, part))
-            if part >= 0:
-                slots.append((part, part + width))
+    for kind, width, (req, g, tok0, pos0, npos, kb, ke, part) in results:
+        assert kb % 64 == 0 and kb < ke and npos * G <= width
+        assert tok0 == starts[req] + pos0 - reqs[req][1]
+        assert ke <= pos0 + npos and ke <= reqs[req][0] + reqs[req][1]
+        for i in range(npos):
+            cover[(tok0 + i, g)].append((kb, ke, part))
+        if part >= 0:
+            slots.append((part, part + width))
     for t in range(starts[-1]):
         pos = toks[t][0]
         for g in range(nkv):
@@ -84,12 +107,6 @@ def check(plan, shape, reqs):
         assert n > 1 and stride in (16, tile_cols) and npos * G <= stride
         want += [gi * 16 + cb for cb in range(-(-npos * G // 16))]
     assert sorted(u[0] for u in plan["merge"]) == want
-    # units: each tile once, each group of per_unit items once
-    units = [u[0] for u in plan["unit"]]
-    tiles = sorted(u for u in units if u >= 0)
-    groups = sorted(-1 - u for u in units if u < 0)
-    assert tiles == list(range(len(plan["tile"])))
-    assert groups == list(range(-(-len(plan["item"]) // per_unit)))
 
 
 SHAPES = {"tiny": (256, 4, 2, 64, 688), "8b": (4096, 32, 8, 128, 14336), "70b": (8192, 64, 8, 128, 28672),
@@ -105,6 +122,7 @@ SHAPES = {"tiny": (256, 4, 2, 64, 688), "8b": (4096, 32, 8, 128, 14336), "70b": 
     ("g16", [(37, 21), (1, 0), (300, 5), (5, 3)], 8),
     ("g1", [(129, 0), (1, 15), (1, 16), (7, 1000)], 4),
     ("8b", [(33, 0), (32, 40), (31, 1)], 1),
+    ("8b", [(1, 519), (1, 599), (1, 4100), (1, 2049), (1, 8191), (1, 511), (3, 700)], 256),
 ])
 def test_plan_covers_every_key_once(driver, name, reqs, cu):
     plan = run_plan(driver, SHAPES[name], cu, reqs)
