@@ -1,8 +1,9 @@
 // Whole-model iteration: token embedding, a stack of hybrid-batch decoder
 // layers, final RMSNorm, LM head and greedy next-token choice. Every layer is
-// an hb_layer driven through hb_run_iteration; the model adds the embedding
-// gather, the selection of each request's last row, the head GEMM (the layer
-// GEMM with an fp32 store and no residual) and the argmax.
+// an hb_layer; the stack runs through the layer runtime with the batch
+// validated, planned and uploaded once per iteration. The model adds the
+// embedding gather, the selection of each request's last row, the head GEMM
+// (the layer GEMM with an fp32 store and no residual) and the argmax.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -12,6 +13,7 @@
 #include "hb.h"
 #include "hb_kernels.h"
 #include "hb_plan.h"
+#include "hb_runtime.h"
 
 using namespace hb;
 
@@ -140,16 +142,20 @@ hb_status hb_run_model(hb_model* m, const hb_model_batch* b) {
   launch_gather_rows(m->stream, m->embed, m->vocab, b->token_ids, T, H, m->x[0]);
   // hidden states ping-pong between two buffers, or go to the caller's
   // per-layer slices
+  // per-layer slices; every layer reads the one metadata upload
   uint16_t* hs = static_cast<uint16_t*>(b->hidden_states);
+  const size_t nl = m->layers.size();
+  std::vector<const void*> xin(nl);
+  std::vector<void*> xout(nl);
   const uint16_t* cur = m->x[0];
-  for (size_t l = 0; l < m->layers.size(); ++l) {
+  for (size_t l = 0; l < nl; ++l) {
     uint16_t* next = hs ? hs + l * (size_t)T * H : m->x[(cur == m->x[0]) ? 1 : 0];
-    desc.x_in = cur;
-    desc.x_out = next;
-    st = hb_run_iteration(m->layers[l], &desc);
-    if (st != HB_OK) return st;
+    xin[l] = cur;
+    xout[l] = next;
     cur = next;
   }
+  st = run_layer_stack(m->layers.data(), (int)nl, &desc, xin.data(), xout.data());
+  if (st != HB_OK) return st;
   launch_gather_rows(m->stream, cur, T, m->rows_dev, R, H, m->last);
   launch_rmsnorm(m->stream, m->last, false, m->g_final, m->normed, R, H, c.rms_eps);
 

@@ -14,6 +14,7 @@
 #include "hb.h"
 #include "hb_kernels.h"
 #include "hb_plan.h"
+#include "hb_runtime.h"
 
 using namespace hb;
 
@@ -295,6 +296,7 @@ hb_status check_hip(const char* what) {
 // A planned batch made ready to launch: GEMM shapes and plans, workspaces
 // sized, metadata uploaded (the layer's stream waits for the copy).
 struct Prepared {
+  const Plan* plan = nullptr;  // the batch's plan (metadata offsets, T)
   GemmArgs gq, go, gu, gd;
   GemmPlan pq, po, pu, pd;
   const int32_t* meta = nullptr;
@@ -346,10 +348,10 @@ void layer_gemms(const Dims& d, int T, const hb_layer* L, const hb_batch_desc* d
   gd.R = L->h2;
 }
 
-// Everything of an iteration up to its launches, for the batch in L->plan.
-hb_status prepare_layer(hb_layer* L, const hb_batch_desc* desc, Prepared* pp) {
+// An iteration's GEMM shapes and plans and the layer's buffers sized, for
+// the batch planned in p (the metadata upload is left to the caller).
+hb_status prepare_gemms(hb_layer* L, const hb_batch_desc* desc, const Plan& p, Prepared* pp) {
   const Dims& d = L->d;
-  Plan& p = L->plan;
   const int T = p.T;
   GemmArgs g[HB_GEMM_COUNT];
   layer_gemms(d, T, L, desc, g);
@@ -375,7 +377,15 @@ hb_status prepare_layer(hb_layer* L, const hb_batch_desc* desc, Prepared* pp) {
   pp->timing_mask = L->timing_mask;
   L->last_plans[HB_GEMM_QKV] = pq; L->last_plans[HB_GEMM_O] = po;
   L->last_plans[HB_GEMM_GATE_UP] = pu; L->last_plans[HB_GEMM_DOWN] = pd;
-  return stage_upload(L, p.meta.data(), p.meta.size(), &pp->meta, &pp->slot);
+  pp->plan = &p;
+  return HB_OK;
+}
+
+// Everything of an iteration up to its launches, for the batch in L->plan.
+hb_status prepare_layer(hb_layer* L, const hb_batch_desc* desc, Prepared* pp) {
+  const hb_status st = prepare_gemms(L, desc, L->plan, pp);
+  if (st != HB_OK) return st;
+  return stage_upload(L, L->plan.meta.data(), L->plan.meta.size(), &pp->meta, &pp->slot);
 }
 
 // The launches of a prepared iteration.
@@ -390,7 +400,7 @@ hb_status launch_layer(hb_layer* L, const hb_batch_desc* desc, const Prepared& p
   } consumed{L, pp.slot};
   const uint32_t tm = pp.timing_mask;
   const Dims& d = L->d;
-  const Plan& p = L->plan;
+  const Plan& p = *pp.plan;
   const int T = p.T;
   hipStream_t s = L->stream;
   const uint16_t* x_in = static_cast<const uint16_t*>(desc->x_in);
@@ -531,6 +541,43 @@ struct SplitMix {
 };
 
 }  // namespace
+
+namespace hb {
+
+// The metadata goes through the first layer's ring; its slot is released
+// after the last layer's kernels.
+hb_status run_layer_stack(hb_layer* const* layers, int n, const hb_batch_desc* desc, const void* const* x_in,
+                          void* const* x_out) {
+  if (n < 1 || !layers || !layers[0]) return fail(HB_ERR_INVALID, "empty layer stack");
+  hb_layer* L0 = layers[0];
+  hb_status st = check_batch(L0->d, L0->pool.num_blocks, desc, &L0->marks);
+  if (st != HB_OK) return st;
+  if (desc->n_requests == 0) return HB_OK;
+  build_plan(L0->d, desc, L0->cu_count, &L0->plan, L0->plan_opt);
+  const int32_t* meta = nullptr;
+  int slot = -1;
+  st = stage_upload(L0, L0->plan.meta.data(), L0->plan.meta.size(), &meta, &slot);
+  if (st != HB_OK) return st;
+  for (int l = 0; l < n && st == HB_OK; ++l) {
+    if (layers[l]->stream != L0->stream) {
+      st = fail(HB_ERR_INVALID, "layer %d runs on another stream", l);
+      break;
+    }
+    hb_batch_desc dl = *desc;
+    dl.x_in = x_in[l];
+    dl.x_out = x_out[l];
+    Prepared pp;
+    st = prepare_gemms(layers[l], &dl, L0->plan, &pp);
+    if (st != HB_OK) break;
+    pp.meta = meta;
+    pp.slot = -1;
+    st = launch_layer(layers[l], &dl, pp);
+  }
+  const hb_status sc = stage_consumed(L0, slot);
+  return st != HB_OK ? st : sc;
+}
+
+}  // namespace hb
 
 extern "C" {
 
@@ -682,6 +729,7 @@ hb_status hb_run_iteration_noalloc(hb_layer* L, const hb_batch_desc* desc) {
   L->na_pending = true;
   pp.gq = g[HB_GEMM_QKV]; pp.go = g[HB_GEMM_O]; pp.gu = g[HB_GEMM_GATE_UP]; pp.gd = g[HB_GEMM_DOWN];
   pp.pq = pl[HB_GEMM_QKV]; pp.po = pl[HB_GEMM_O]; pp.pu = pl[HB_GEMM_GATE_UP]; pp.pd = pl[HB_GEMM_DOWN];
+  pp.plan = &p;
   pp.meta = reinterpret_cast<const int32_t*>(L->scratch);
   pp.slot = -1;
   pp.splitk = reinterpret_cast<float*>(L->scratch + off_splitk);
