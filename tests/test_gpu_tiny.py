@@ -69,8 +69,11 @@ SMALL_SHAPES = [
 @pytest.mark.parametrize("shape", SMALL_SHAPES, ids=lambda s: s.name)
 def test_small_shapes_parity(hb, shape):
     # short chunks (wave items), long chunks (workgroup tiles, split over a
-    # long context), decodes on block edges and with a long context
-    lens = [(37, 21), (1, 0), (1, 15), (1, 16), (100, 0), (1, 300), (5, 3), (300, 1200), (1, 2000)]
+    # long context), decodes on block edges and with long contexts: 2001 keys
+    # (four waves of one workgroup combined in LDS), 520 (the same, one wave
+    # with an empty range) and 3001 (two such workgroups and a merge)
+    lens = [(37, 21), (1, 0), (1, 15), (1, 16), (100, 0), (1, 300), (5, 3), (300, 1200), (1, 2000), (1, 519),
+            (1, 3000)]
     b = make_batch(shape, lens, seed=77, num_blocks=512)
     dl, w = _setup(hb, b)
     y = _run(dl, b)
