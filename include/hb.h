@@ -84,12 +84,17 @@ typedef struct {
 } hb_layer_weights;
 
 /* Paged KV cache of one layer: device bf16, caller-owned.
- *   k_pool  [num_blocks][n_kv_heads][16][head_dim]        K of slot s at [..][s][d]
- *   v_pool  [num_blocks][n_kv_heads][2][head_dim][8]      V of slot s at [..][s/8][d][s%8]
+ *   k_pool  [num_blocks][n_kv_heads][2][head_dim/8][8][8]  K of slot s at
+ *           [..][(s/4)%2][d/8][4(s/8) + s%4][d%8]
+ *   v_pool  [num_blocks][n_kv_heads][2][head_dim][8]       V of slot s at [..][s/8][d][s%8]
  * Position p of a request lives in block block_table[p / 16], slot p % 16.
- * Keys are stored after RoPE. Within a block, V is split into two halves of
- * eight slots, dimension-major inside a half: the eight keys of one dimension
- * are one 16-byte operand of the PV product. */
+ * Keys are stored after RoPE. Both layouts keep a block of one kv head
+ * (16 slots x head_dim) contiguous, 16 x head_dim x 2 bytes. K groups slots
+ * 0-3, 8-11 and 4-7, 12-15 (the keys one score product takes), and stores
+ * each group eight dimensions at a time, so a 16-byte read of eight
+ * dimensions of eight keys is one 128-byte line. V is split into two halves
+ * of eight slots, dimension-major inside a half: the eight keys of one
+ * dimension are one 16-byte operand of the PV product. */
 typedef struct {
   void *k_pool, *v_pool;
   int32_t num_blocks;

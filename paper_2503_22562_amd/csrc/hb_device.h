@@ -38,6 +38,17 @@ __device__ __forceinline__ void st8(void* p, u32x2 v) { *reinterpret_cast<u32x2*
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Element offset of (key slot s, dimension d) in one K block of one kv head.
+// The block is stored as [2][hd / 8][8][8]: slots 0-3 and 8-11 form group 0,
+// slots 4-7 and 12-15 group 1, and within a group each 8-dimension chunk
+// holds its 8 slots x 8 dimensions (128 bytes). One score MFMA of an
+// attention step takes exactly one group's keys, so its 16-byte lane loads
+// read whole 128-byte lines.
+__host__ __device__ __forceinline__ int k_block_offset(int s, int d, int hd) {
+  const int g = (s >> 2) & 1, j = ((s >> 3) << 2) | (s & 3);
+  return ((g * (hd >> 3) + (d >> 3)) * 8 + j) * 8 + (d & 7);
+}
+
 // D(16x16) += A(16x32) * B(32x16), bf16 in, fp32 accumulate.
 // Operand registers: lane l holds row (A) / column (B) l % 16 and eight
 // consecutive k values of k-group l / 16; the result holds column l % 16 and

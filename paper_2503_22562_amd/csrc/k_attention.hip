@@ -7,8 +7,8 @@
 // running maximum needs two cross-lane exchanges per step. The PV product is
 // also transposed, O^T += V^T P^T: the probabilities are reused from the score
 // registers (the MFMA k order only has to agree between its two operands) and
-// the pool's V blocks, grouped by four keys and dimension-major inside a
-// group, supply V^T fragments as 8-byte reads. A query column is one
+// the pool's V blocks, grouped by eight keys and dimension-major inside a
+// group, supply V^T fragments as 16-byte reads. A query column is one
 // (position, q head) pair; the G = n_q / n_kv heads of a kv head sit in
 // adjacent columns so each K/V byte serves all of them.
 //
@@ -16,10 +16,12 @@
 // two workgroups per CU, so a compute-bound tile and a bandwidth-bound item
 // group can run side by side on one CU):
 //  * chunk tiles: 128 columns (4 waves x 32) of one request and kv head over a
-//    key range; 32-key K/V steps (two pool blocks) are copied into a 4-stage
-//    LDS ring by global-to-LDS loads and every wave reads them from there
-//    (K rows XOR-swizzled in 16-byte chunks so fragment reads do not collide
-//    in banks). Compute-bound: 32 MFMAs per wave per step.
+//    key range; 32-key K/V steps (two pool blocks) are copied as stored into
+//    a 4-stage LDS ring by global-to-LDS loads and every wave reads them from
+//    there (the pool's K layout puts a fragment read's 8 keys of one
+//    dimension chunk in one 128-byte line; the second block sits 128 bytes
+//    off, so reads do not collide in banks). Compute-bound: 32 MFMAs per wave
+//    per step.
 //  * wave items: 16 columns (decodes, short chunks) per wave, four per
 //    workgroup; each wave streams its K/V straight into registers, the next
 //    32-key step loading while the current one is multiplied. HBM-bound.
@@ -159,13 +161,14 @@ __device__ __forceinline__ void wave_load(WaveStep<HD>& st, const AttnArgs& a, i
                                           int grp) {
   const size_t blk_stride = (size_t)a.nkv * 16 * HD;
   const size_t head_off = (size_t)g * 16 * HD;
-  // K: this lane's rows (keys 8 (col / 4) + 4 b + col % 4) lie in block col / 8
-  const uint16_t* K = a.k_pool + (size_t)((col >> 3) ? id1 : id0) * blk_stride + head_off +
-                      (8 * ((col >> 2) & 1) + (col & 3)) * HD + 8 * grp;
+  // K: this lane's key (8 (col / 4) + 4 b + col % 4 of the step) is slot
+  // col % 8 of slot group b in block col / 8, and its dimensions 32 kc +
+  // 8 grp .. + 7 are chunk 4 kc + grp: a load's lanes cover whole lines
+  const uint16_t* K = a.k_pool + (size_t)((col >> 3) ? id1 : id0) * blk_stride + head_off + (8 * grp + (col & 7)) * 8;
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
-    for (int kc = 0; kc < HD / 32; ++kc) st.k[b][kc] = ld16_stream(K + 4 * b * HD + 32 * kc);
+    for (int kc = 0; kc < HD / 32; ++kc) st.k[b][kc] = ld16_stream(K + (b * (HD / 8) + 4 * kc) * 64);
   // V: keys 8 grp..+7 are half grp % 2 of block grp / 2
   const uint16_t* V = a.v_pool + (size_t)((grp >> 1) ? id1 : id0) * blk_stride + head_off +
                       ((grp & 1) * HD + col) * 8;
@@ -389,73 +392,54 @@ constexpr int TSTAGES = 4;   // LDS ring depth of the tile path
 template <int HD>
 struct TileGeom {
   static constexpr int BLK = 16 * HD * 2;        // bytes of one K (or V) block of one head
-  static constexpr int ROW = HD * 2;             // bytes of one key row
   static constexpr int LOADS = BLK / 1024;       // 1-KB loads per block
-  static constexpr int KEYS_PER_LOAD = 1024 / ROW;
-  static constexpr int CHUNKS = ROW / 16;        // 16-byte chunks per key row
-  // Both V blocks are copied as stored ([half][dim][8 keys] each), so the
-  // 16 bytes of keys 8 g..8 g+7 of dim d sit at g * HD * 16 + d * 16.
-  static constexpr int STAGE = 4 * BLK;  // 2 K blocks then 2 V blocks
-  // 16-byte chunk c of K row r of block b is stored at chunk c ^ kswz(b, r).
-  // The 16 rows one fragment read touches (rows 0-3 and 8-11, or 4-7 and
-  // 12-15, of both blocks) then cover all bank positions; rows r and r + 4
-  // share the pattern, so the two score MFMAs' reads differ by a constant.
-  static constexpr __host__ __device__ int kswz(int b, int r) {
-    return HD == 128 ? ((r & 11) ^ (b << 2)) : (((r >> 1) & 1) | (((r >> 3) & 1) << 1) | (b << 2));
-  }
+  // Blocks are copied as stored: K [group][chunk][8 keys][8 dims], V
+  // [half][dim][8 keys]. The second K block sits 128 bytes further on, so
+  // the two blocks' halves of a fragment read fall in different banks.
+  static constexpr int KPAD = 128;
+  static constexpr int STAGE = 4 * BLK + KPAD;  // K of 2 blocks, then V of 2 blocks
+  static constexpr __host__ __device__ int off(int b) { return b * BLK + (b > 0 ? KPAD : 0); }
 };
 
-// One step is four blocks in the stage: K of the two pool blocks (rows
-// chunk-swizzled), then their V. Wave b copies stage
-// block b: the K (b = 0, 1) or V (b = 2, 3) of pool block b & 1.
+// One step is four blocks in the stage: K of the two pool blocks, then their
+// V. Wave b copies stage block b: the K (b = 0, 1) or V (b = 2, 3) of pool
+// block b & 1.
 template <int HD>
 __device__ __forceinline__ void tile_issue(uint8_t* stage, const AttnArgs& a, int id, int g, int wave, int lane) {
   using TG = TileGeom<HD>;
   typedef __attribute__((address_space(3))) void* lds_ptr;
   const int b = wave;
-  // a buffer resource over this wave's 4-KB block (K or V of pool block b & 1):
+  // a buffer resource over this wave's block (K or V of pool block b & 1):
   // the loads then carry only a lane offset and a scalar offset
   const uint16_t* blk = (b < 2 ? a.k_pool : a.v_pool) + ((size_t)id * a.nkv + g) * 16 * HD;
   const __amdgpu_buffer_rsrc_t r =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(blk), (short)0, TG::BLK, 0x00020000);
-  uint8_t* dst = stage + b * TG::BLK;  // K of both blocks, then V of both
-  if (b < 2) {
-    const int kk_lane = lane / TG::CHUNKS, pc = lane % TG::CHUNKS;
+  uint8_t* dst = stage + TG::off(b);
 #pragma unroll
-    for (int i = 0; i < TG::LOADS; ++i) {
-      const int kk = i * TG::KEYS_PER_LOAD + kk_lane;
-      const uint32_t voff = 2u * (uint32_t)(kk_lane * HD + 8 * (pc ^ TG::kswz(b, kk)));
-      uint8_t* d = dst + i * 1024;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)d, 16, voff, (uint32_t)(i * 1024), 0, 0);
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < TG::LOADS; ++i) {
-      uint8_t* d = dst + i * 1024;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)d, 16, (uint32_t)(lane * 16), (uint32_t)(i * 1024), 0, 0);
-    }
+  for (int i = 0; i < TG::LOADS; ++i) {
+    uint8_t* d = dst + i * 1024;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)d, 16, (uint32_t)(lane * 16), (uint32_t)(i * 1024), 0, 0);
   }
 }
 
 // Fragments of one step from a stage. K: for score MFMA b, the lane's key
-// row, at k_lane (block and row of key 8 (col / 4) + col % 4, OR-ed with the
-// lane's swizzled chunk (grp ^ kswz) * 16; 4 rows further for b = 1; chunk
-// 4 kc + grp is the XOR with kc * 64). V: keys 8 grp..+7 of dims 16 dt + col
+// (slot col % 8 of slot group b in block col / 8) and dimension chunk
+// 4 kc + grp: k_lane = block offset + (8 grp + col % 8) * 16, plus
+// (b hd/8 + 4 kc) * 128. V: keys 8 grp..+7 of dims 16 dt + col
 // (v_lane = grp * HD * 16 + col * 16).
 template <int HD>
 __device__ __forceinline__ void tile_read_k(bf16x8 (&kf)[2][HD / 32], const uint8_t* st, int k_lane) {
-  using TG = TileGeom<HD>;
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
     for (int kc = 0; kc < HD / 32; ++kc)
-      kf[b][kc] = as_bf16x8(*reinterpret_cast<const u32x4*>(st + 4 * b * TG::ROW + (k_lane ^ (kc << 6))));
+      kf[b][kc] = as_bf16x8(*reinterpret_cast<const u32x4*>(st + k_lane + (b * (HD / 8) + 4 * kc) * 128));
 }
 
 template <int HD>
 __device__ __forceinline__ void tile_read_v(u32x4 (&vf)[HD / 16], const uint8_t* st, int v_lane) {
   using TG = TileGeom<HD>;
-  const uint8_t* vs = st + 2 * TG::BLK + v_lane;
+  const uint8_t* vs = st + TG::off(2) + v_lane;
 #pragma unroll
   for (int dt = 0; dt < HD / 16; ++dt) vf[dt] = *reinterpret_cast<const u32x4*>(vs + dt * 256);
 }
@@ -619,8 +603,7 @@ __device__ __forceinline__ void tile_unit(const AttnArgs& a, const AttnItem& it,
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct) { m[ct] = NEG_BIG; l[ct] = 0.f; }
 
-  const int k_row = 8 * ((col >> 2) & 1) + (col & 3);  // row of key 8 (col / 4) + col % 4 in block col / 8
-  const int k_lane = (col >> 3) * TG::BLK + k_row * TG::ROW + ((grp ^ TG::kswz(col >> 3, k_row)) << 4);
+  const int k_lane = TG::off(col >> 3) + (8 * grp + (col & 7)) * 16;
   const int v_lane = grp * HD * 16 + col * 16;
   // prologue: steps 0..TSTAGES-2 in flight, scores of step 0
   int next_id = const_load(btab + min(kb0 + (wave & 1), kb_last));

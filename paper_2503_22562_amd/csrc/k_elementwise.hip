@@ -99,7 +99,7 @@ __global__ __launch_bounds__(256) void append_kv_kernel(const uint16_t* __restri
   const int n = nkv * hd;
   for (int idx = threadIdx.x; idx < n; idx += 256) {
     const int g = idx / hd, d = idx - g * hd;
-    k_pool[(((size_t)blk * nkv + g) * 16 + slot) * hd + d] = k[(size_t)t * n + idx];
+    k_pool[((size_t)blk * nkv + g) * 16 * hd + k_block_offset(slot, d, hd)] = k[(size_t)t * n + idx];
     v_pool[((size_t)blk * nkv + g) * 16 * hd + ((slot >> 3) * hd + d) * 8 + (slot & 7)] = v[(size_t)t * n + idx];
   }
 }

@@ -316,15 +316,16 @@ __device__ __forceinline__ void qkv_rope_row(const GemmArgs& a, const f32x4 (&ac
       }
       const u32x2 wl = {pack_bf16x2(rl[0], rl[1]), pack_bf16x2(rl[2], rl[3])};
       const u32x2 wh = {pack_bf16x2(rh[0], rh[1]), pack_bf16x2(rh[2], rh[3])};
-      uint16_t* dst;
       if (n < a.nq * HD) {
-        dst = reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + (n - j);
+        uint16_t* dst = reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + (n - j);
+        st8(dst + j, wl);
+        st8(dst + HALF + j, wh);
       } else {
         const int g = (n - a.nq * HD) / HD;
-        dst = a.k_pool + (((size_t)blk * a.nkv + g) * 16 + slot) * HD;
+        uint16_t* kb = a.k_pool + ((size_t)blk * a.nkv + g) * 16 * HD;
+        st8(kb + k_block_offset(slot, j, HD), wl);
+        st8(kb + k_block_offset(slot, HALF + j, HD), wh);
       }
-      st8(dst + j, wl);
-      st8(dst + HALF + j, wh);
     } else {
       const int g = (n - qk_end) / HD, d = n % HD;
       uint16_t* vp = a.v_pool + ((size_t)blk * a.nkv + g) * 16 * HD + ((slot >> 3) * HD + d) * 8 + (slot & 7);
@@ -624,15 +625,18 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, const fl
         rl[e] = lo[e] * c - hi[e] * sn;
         rh[e] = hi[e] * c + lo[e] * sn;
       }
-      uint16_t* dst;
+      const u32x2 wl = {pack_bf16x2(rl[0], rl[1]), pack_bf16x2(rl[2], rl[3])};
+      const u32x2 wh = {pack_bf16x2(rh[0], rh[1]), pack_bf16x2(rh[2], rh[3])};
       if (h < a.nq) {
-        dst = reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + h * hd;
+        uint16_t* dst = reinterpret_cast<uint16_t*>(a.C) + (size_t)m * a.ldc + h * hd;
+        st8(dst + j, wl);
+        st8(dst + half + j, wh);
       } else {
-        const int slotm = a.tok_slot[m];
-        dst = a.k_pool + (((size_t)(slotm >> 4) * a.nkv + (h - a.nq)) * 16 + (slotm & 15)) * hd;
+        const int slotm = a.tok_slot[m], slot = slotm & 15;
+        uint16_t* kb = a.k_pool + ((size_t)(slotm >> 4) * a.nkv + (h - a.nq)) * 16 * hd;
+        st8(kb + k_block_offset(slot, j, hd), wl);
+        st8(kb + k_block_offset(slot, half + j, hd), wh);
       }
-      st8(dst + j, u32x2{pack_bf16x2(rl[0], rl[1]), pack_bf16x2(rl[2], rl[3])});
-      st8(dst + half + j, u32x2{pack_bf16x2(rh[0], rh[1]), pack_bf16x2(rh[2], rh[3])});
       return;
     }
     const int dblocks = hd / 32;

@@ -26,6 +26,16 @@ def to_device_bf16(bits: np.ndarray, device: str = "cuda"):
     return torch.from_numpy(b).to(device).view(torch.bfloat16)
 
 
+def k_by_slot(k_bits: np.ndarray) -> np.ndarray:
+    """View a K pool [blocks][kv][16][hd] whose blocks are stored as
+    [slot group 2][hd / 8][8 slots][8 dims] (group 0: slots 0-3 and 8-11,
+    group 1: slots 4-7 and 12-15) as [blocks][kv][slot][hd]."""
+    nb, nkv, _, hd = k_bits.shape
+    x = k_bits.reshape(nb, nkv, 2, hd // 8, 8, 8).transpose(0, 1, 2, 4, 3, 5).reshape(nb, nkv, 2, 8, hd)
+    s = np.arange(16)
+    return x[:, :, (s >> 2) & 1, ((s >> 3) << 2) | (s & 3), :]
+
+
 def v_by_slot(v_bits: np.ndarray) -> np.ndarray:
     """View a V pool [blocks][kv][2][hd][8] as [blocks][kv][slot][hd]."""
     nb, nkv, _, hd, _ = v_bits.shape

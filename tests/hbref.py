@@ -143,7 +143,7 @@ def check_attention_kernel(dl, batch, rows, q_bits, o_bits, what="attention"):
     probability rounding, for the fp32 exponentials and sums).
     q_bits, o_bits: uint16 [len(rows)][n_q head_dim] of the sampled rows."""
     import torch
-    from paper_2503_22562_amd.harness import bf16_bits, v_by_slot
+    from paper_2503_22562_amd.harness import bf16_bits, k_by_slot, v_by_slot
     shape = batch.shape
     nq, nkv, hd = shape.n_q_heads, shape.n_kv_heads, shape.head_dim
     rows = np.asarray(rows)
@@ -158,7 +158,7 @@ def check_attention_kernel(dl, batch, rows, q_bits, o_bits, what="attention"):
         kv = req.context_len + req.chunk_len
         nb = -(-kv // 16)
         idx = torch.from_numpy(np.asarray(req.block_table[:nb], dtype=np.int64)).to(dl.k_pool.device)
-        kb = bf16_bits(dl.k_pool.index_select(0, idx))                  # [nb][nkv][16][hd]
+        kb = k_by_slot(bf16_bits(dl.k_pool.index_select(0, idx)))       # [nb][nkv][16][hd]
         vb = v_by_slot(bf16_bits(dl.v_pool.index_select(0, idx)))       # [nb][nkv][16][hd]
         k = oracle.bf16_bits_to_f64(kb.transpose(0, 2, 1, 3).reshape(nb * 16, nkv, hd)[:kv])
         v = oracle.bf16_bits_to_f64(vb.transpose(0, 2, 1, 3).reshape(nb * 16, nkv, hd)[:kv])

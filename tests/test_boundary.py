@@ -205,3 +205,21 @@ def test_gemm_plans_host_only(H):
 
 def test_model_layer_of_null_model(H):
     assert not H.load().hb_model_layer(None, 0)
+
+
+@pytest.mark.parametrize("hd", [64, 128])
+def test_pool_layout_views(hd):
+    """The pool layouts hb.h documents, written out element by element, are
+    what the harness's per-slot views undo: K of slot s, dimension d at
+    [(s/4)%2][d/8][4(s/8) + s%4][d%8]; V at [s/8][d][s%8]."""
+    from paper_2503_22562_amd.harness import k_by_slot, v_by_slot
+    nb, nkv = 3, 2
+    want = np.random.default_rng(hd).integers(0, 1 << 16, (nb, nkv, 16, hd)).astype(np.uint16)
+    k = np.zeros((nb, nkv, 2, hd // 8, 8, 8), np.uint16)
+    v = np.zeros((nb, nkv, 2, hd, 8), np.uint16)
+    for s in range(16):
+        for d in range(hd):
+            k[:, :, (s // 4) % 2, d // 8, 4 * (s // 8) + s % 4, d % 8] = want[:, :, s, d]
+            v[:, :, s // 8, d, s % 8] = want[:, :, s, d]
+    assert np.array_equal(k_by_slot(k.reshape(nb, nkv, 16, hd)), want)
+    assert np.array_equal(v_by_slot(v), want)

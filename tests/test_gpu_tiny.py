@@ -98,8 +98,8 @@ def _expected_slots(batch, which):
 
 def _pool_bits(dl):
     """K and V pools as [block][kv head][slot][head_dim] bit patterns."""
-    from paper_2503_22562_amd.harness import bf16_bits, v_by_slot
-    return bf16_bits(dl.k_pool), v_by_slot(bf16_bits(dl.v_pool))
+    from paper_2503_22562_amd.harness import bf16_bits, k_by_slot, v_by_slot
+    return k_by_slot(bf16_bits(dl.k_pool)), v_by_slot(bf16_bits(dl.v_pool))
 
 
 def test_append_kv_placement_bit_exact(hb):
