@@ -187,18 +187,19 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p,
     for (int i0 = 0; i0 < c; i0 += w) (is_tile(r) ? tile_keys : item_keys) += (double)d.nkv * (x + std::min(c, i0 + w));
   }
   // split lengths (multiples of 64 keys): about one round of tile workgroups
-  // (each split also writes kTileCols columns of fp32 partials) and about four
-  // items per wave slot (8 per compute unit), so long decodes do not set the
-  // finishing time. When both kinds are present, tiles run beside the
-  // bandwidth-bound items for the whole launch, so they are split less
-  // (4096 keys), and items are at least 512 keys: both halve the partial
-  // results the merge must read (measured on MI355X over chunk/decode mixes).
+  // (each split also writes kTileCols columns of fp32 partials), and for
+  // items about two wave slots' worth of keys per wave (4 per compute unit),
+  // at least 1024 keys, so a merged unit spans up to 4 S_i keys and most
+  // decodes need no merge kernel. When both kinds are present, tiles run
+  // beside the bandwidth-bound items for the whole launch, so they are split
+  // less (4096 keys). Measured on MI355X over chunk/decode mixes (item split
+  // 512 .. 4096, tile split 1024 .. 4096).
   const int cus = std::max(1, cu_count);
   const bool mixed = tile_keys > 0 && item_keys > 0;
   const int S_t = opt.split_tile > 0 ? round_up(opt.split_tile, 64)
                                      : std::max(mixed ? 4096 : 1024, round_up((int64_t)(tile_keys / (1.0 * cus)) + 1, 64));
   const int S_i = opt.split_item > 0 ? round_up(opt.split_item, 64)
-                                     : std::max(512, round_up((int64_t)(item_keys / (32.0 * cus)) + 1, 64));
+                                     : std::max(1024, round_up((int64_t)(item_keys / (16.0 * cus)) + 1, 64));
   p->split_tile = S_t;
   p->split_item = S_i;
 

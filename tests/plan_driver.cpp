@@ -1,13 +1,14 @@
 // Test driver for the host planner: reads a batch from stdin, prints the plan.
-// Input: "H nq nkv hd F cu R" then R lines "chunk ctx nblocks id...".
+// Input: "H nq nkv hd F cu R split_item" then R lines "chunk ctx nblocks id..."
+// (split_item 0: the planner's own choice).
 #include <cstdio>
 #include <vector>
 
 #include "hb_plan.h"
 
 int main() {
-  int H, nq, nkv, hd, F, cu, R;
-  if (scanf("%d %d %d %d %d %d %d", &H, &nq, &nkv, &hd, &F, &cu, &R) != 7) return 2;
+  int H, nq, nkv, hd, F, cu, R, split_item;
+  if (scanf("%d %d %d %d %d %d %d %d", &H, &nq, &nkv, &hd, &F, &cu, &R, &split_item) != 8) return 2;
   std::vector<hb_request> reqs(R);
   std::vector<std::vector<int32_t>> tables(R);
   int T = 0;
@@ -26,7 +27,9 @@ int main() {
   hb_batch_desc desc{R, reqs.data(), (void*)0x1000, (void*)0x80000000, HB_OUT_F32};
   if (hb::check_batch(d, 1 << 30, &desc, nullptr) != HB_OK) return 4;
   hb::Plan p;
-  hb::build_plan(d, &desc, cu, &p);
+  hb::PlanOptions opt;
+  opt.split_item = split_item;
+  hb::build_plan(d, &desc, cu, &p, opt);
   const int32_t* m = p.meta.data();
   printf("T %d %d %d %d\n", p.T, p.split_tile, p.split_item, p.n_slots);
   printf("geom %d %d\n", hb::kTileCols, hb::kItemsPerUnit);

@@ -66,15 +66,19 @@ SMALL_SHAPES = [
 ]
 
 
+@pytest.mark.parametrize("split_item", [0, 512], ids=["item-split-auto", "item-split-512"])
 @pytest.mark.parametrize("shape", SMALL_SHAPES, ids=lambda s: s.name)
-def test_small_shapes_parity(hb, shape):
+def test_small_shapes_parity(hb, monkeypatch, shape, split_item):
     # short chunks (wave items), long chunks (workgroup tiles, split over a
-    # long context), decodes on block edges and with long contexts: 2001 keys
-    # (four waves of one workgroup combined in LDS), 520 (the same, one wave
-    # with an empty range) and 3001 (two such workgroups and a merge)
+    # long context), decodes on block edges and with long contexts, whose key
+    # ranges run as the four waves of one workgroup combined in LDS or over
+    # several such workgroups and a merge; with a 512-key item split, 520 keys
+    # leave one wave of a workgroup an empty range
+    if split_item:
+        monkeypatch.setenv("HB_ATTN_SPLIT_ITEM", str(split_item))
     lens = [(37, 21), (1, 0), (1, 15), (1, 16), (100, 0), (1, 300), (5, 3), (300, 1200), (1, 2000), (1, 519),
-            (1, 3000)]
-    b = make_batch(shape, lens, seed=77, num_blocks=512)
+            (1, 3000), (1, 5000)]
+    b = make_batch(shape, lens, seed=77, num_blocks=1024)
     dl, w = _setup(hb, b)
     y = _run(dl, b)
     ref = oracle_for_batch(b, oracle.weights_to_f64(w))

@@ -23,9 +23,9 @@ def driver(tmp_path_factory):
     return exe
 
 
-def run_plan(exe, shape, cu, reqs):
+def run_plan(exe, shape, cu, reqs, split_item=0):
     H, nq, nkv, hd, F = shape
-    lines = [f"{H} {nq} {nkv} {hd} {F} {cu} {len(reqs)}"]
+    lines = [f"{H} {nq} {nkv} {hd} {F} {cu} {len(reqs)} {split_item}"]
     nxt = 0
     for c, x in reqs:
         nb = -(-(c + x) // 16)
@@ -127,3 +127,14 @@ SHAPES = {"tiny": (256, 4, 2, 64, 688), "8b": (4096, 32, 8, 128, 14336), "70b": 
 def test_plan_covers_every_key_once(driver, name, reqs, cu):
     plan = run_plan(driver, SHAPES[name], cu, reqs)
     check(plan, SHAPES[name], reqs)
+
+
+def test_plan_merged_units_with_short_item_splits(driver):
+    """A short forced item split: merged workgroups with an empty wave range,
+    and ranges spread over several merged workgroups and a merge group."""
+    reqs = [(1, 519), (1, 599), (1, 4100), (1, 2049), (1, 8191), (1, 511), (3, 700), (512, 3000)]
+    plan = run_plan(driver, SHAPES["8b"], 256, reqs, split_item=512)
+    check(plan, SHAPES["8b"], reqs)
+    merged = [(-1 - u[0]) & ~(1 << 29) for u in plan["unit"] if u[0] < 0 and (-1 - u[0]) & (1 << 29)]
+    assert any(it[5] == it[6] for v in merged for it in plan["item"][4 * v:4 * v + 4]), "no empty wave range"
+    assert any(g[2] == 16 for g in plan["group"]), "no merge group of item workgroups"
