@@ -66,16 +66,20 @@ SMALL_SHAPES = [
 ]
 
 
-@pytest.mark.parametrize("split_item", [0, 512], ids=["item-split-auto", "item-split-512"])
+@pytest.mark.parametrize("splits", [(0, 0), (512, 256)], ids=["splits-auto", "item-512-tile-256"])
 @pytest.mark.parametrize("shape", SMALL_SHAPES, ids=lambda s: s.name)
-def test_small_shapes_parity(hb, monkeypatch, shape, split_item):
+def test_small_shapes_parity(hb, monkeypatch, shape, splits):
     # short chunks (wave items), long chunks (workgroup tiles, split over a
     # long context), decodes on block edges and with long contexts, whose key
     # ranges run as the four waves of one workgroup combined in LDS or over
-    # several such workgroups and a merge; with a 512-key item split, 520 keys
-    # leave one wave of a workgroup an empty range
+    # several such workgroups and a merge. Forced short splits: 520 keys leave
+    # one wave of a workgroup an empty range, and the 300-token chunk's tiles
+    # run in 256-key splits, the later ones past the first rows' positions
+    split_item, split_tile = splits
     if split_item:
         monkeypatch.setenv("HB_ATTN_SPLIT_ITEM", str(split_item))
+    if split_tile:
+        monkeypatch.setenv("HB_ATTN_SPLIT_TILE", str(split_tile))
     lens = [(37, 21), (1, 0), (1, 15), (1, 16), (100, 0), (1, 300), (5, 3), (300, 1200), (1, 2000), (1, 519),
             (1, 3000), (1, 5000)]
     b = make_batch(shape, lens, seed=77, num_blocks=1024)
