@@ -544,34 +544,36 @@ struct SplitMix {
 
 namespace hb {
 
-// The metadata goes through the first layer's ring; its slot is released
-// after the last layer's kernels.
+// Every layer is checked and its buffers sized before anything is enqueued,
+// so a failure leaves every pool untouched. The metadata goes through the
+// first layer's ring; its slot is released after the last layer's kernels.
 hb_status run_layer_stack(hb_layer* const* layers, int n, const hb_batch_desc* desc, const void* const* x_in,
                           void* const* x_out) {
-  if (n < 1 || !layers || !layers[0]) return fail(HB_ERR_INVALID, "empty layer stack");
+  if (n < 1 || !layers || !x_in || !x_out) return fail(HB_ERR_INVALID, "empty layer stack");
+  for (int l = 0; l < n; ++l)
+    if (!layers[l] || layers[l]->stream != layers[0]->stream)
+      return fail(HB_ERR_INVALID, "layer %d is null or runs on another stream", l);
   hb_layer* L0 = layers[0];
   hb_status st = check_batch(L0->d, L0->pool.num_blocks, desc, &L0->marks);
   if (st != HB_OK) return st;
   if (desc->n_requests == 0) return HB_OK;
   build_plan(L0->d, desc, L0->cu_count, &L0->plan, L0->plan_opt);
+  std::vector<hb_batch_desc> dl(n, *desc);
+  std::vector<Prepared> pp(n);
+  for (int l = 0; l < n; ++l) {
+    dl[l].x_in = x_in[l];
+    dl[l].x_out = x_out[l];
+    st = prepare_gemms(layers[l], &dl[l], L0->plan, &pp[l]);
+    if (st != HB_OK) return st;
+  }
   const int32_t* meta = nullptr;
   int slot = -1;
   st = stage_upload(L0, L0->plan.meta.data(), L0->plan.meta.size(), &meta, &slot);
   if (st != HB_OK) return st;
   for (int l = 0; l < n && st == HB_OK; ++l) {
-    if (layers[l]->stream != L0->stream) {
-      st = fail(HB_ERR_INVALID, "layer %d runs on another stream", l);
-      break;
-    }
-    hb_batch_desc dl = *desc;
-    dl.x_in = x_in[l];
-    dl.x_out = x_out[l];
-    Prepared pp;
-    st = prepare_gemms(layers[l], &dl, L0->plan, &pp);
-    if (st != HB_OK) break;
-    pp.meta = meta;
-    pp.slot = -1;
-    st = launch_layer(layers[l], &dl, pp);
+    pp[l].meta = meta;
+    pp[l].slot = -1;
+    st = launch_layer(layers[l], &dl[l], pp[l]);
   }
   const hb_status sc = stage_consumed(L0, slot);
   return st != HB_OK ? st : sc;
