@@ -203,3 +203,34 @@ def test_model_token_ids_out_of_range_read_nearest_row(hb):
     _, l_ok = dm.run(_reqs(b), clamped)
     torch.cuda.synchronize()
     assert np.array_equal(got_bad, l_ok.cpu().numpy())
+
+
+def test_model_out_of_memory_leaves_every_pool_untouched(hb, monkeypatch):
+    """A model iteration whose split-K partials do not fit the per-layer
+    device limit (HB_DEVICE_ALLOC_LIMIT, read at creation) fails with
+    HB_ERR_OOM before anything is enqueued: every layer's pool is unchanged.
+    The same model then runs a batch that fits."""
+    import torch
+    from paper_2503_22562_amd import hb as H
+    from paper_2503_22562_amd.harness import bf16_bits
+    shape = LayerShape("m-oom", 2048, 16, 4, 128, 2048, weight_seed=23)
+    mw = make_model_weights(shape, 3, 256)
+    big = make_batch(shape, [(1024, 0), (1, 40)], seed=31, num_blocks=128)
+    # a layer's workspace and attention partials fit; its 8-way split-K
+    # partials (8 x 1025 x 4096 fp32 gate/up partials: 134 MB) do not
+    monkeypatch.setenv("HB_DEVICE_ALLOC_LIMIT", str(100 << 20))
+    monkeypatch.setenv("HB_GEMM_KSPLIT", "8")
+    dm = _device_model(big, mw, big.n_tokens, 4, seed_prior=False)
+    before = [(bf16_bits(k), bf16_bits(v)) for k, v in dm.pools]
+    with pytest.raises(H.HBError) as e:
+        dm.run(_reqs(big), big.token_ids(256))
+    assert e.value.status == H.HB_ERR_OOM
+    torch.cuda.synchronize()
+    for (k, v), (k0, v0) in zip(dm.pools, before):
+        assert np.array_equal(bf16_bits(k), k0) and np.array_equal(bf16_bits(v), v0)
+    small = make_batch(shape, [(8, 0), (1, 3)], seed=32, num_blocks=128)
+    nxt, logits = dm.run(_reqs(small), small.token_ids(256))
+    torch.cuda.synchronize()
+    n = nxt.cpu().numpy()
+    assert n.shape == (2,) and np.all((n >= 0) & (n < 256))
+    assert np.all(np.isfinite(logits.cpu().numpy()))
