@@ -15,6 +15,7 @@ import argparse
 import hashlib
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -512,10 +513,29 @@ def model_iteration(hb, torch, shape, batch_lens, seed, n_layers=32, vocab=12825
                     "compare with the strictest QoS tier's 50 ms"}
 
 
+def gpu_max_clock_mhz():
+    """The first GPU agent's maximum shader clock as rocminfo reports it (None
+    if rocminfo is unavailable)."""
+    try:
+        out = subprocess.run(["rocminfo"], capture_output=True, text=True, timeout=30).stdout
+    except (OSError, subprocess.SubprocessError):
+        return None
+    gpu = False
+    for line in out.splitlines():
+        if "Device Type:" in line:
+            gpu = "GPU" in line
+        elif gpu and "Max Clock Freq. (MHz):" in line:
+            try:
+                return int(line.split(":")[1].split()[0])
+            except (IndexError, ValueError):
+                return None
+    return None
+
+
 def device_info(torch):
     p = torch.cuda.get_device_properties(0)
     return {"name": p.name, "arch": getattr(p, "gcnArchName", None), "compute_units": p.multi_processor_count,
-            "hbm_gib": round(p.total_memory / 2 ** 30, 1),
+            "max_clock_mhz": gpu_max_clock_mhz(), "hbm_gib": round(p.total_memory / 2 ** 30, 1),
             "host_cores": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()}
 
 
