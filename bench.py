@@ -408,11 +408,14 @@ def blas_ceiling(torch, shape, M, steps=10):
         e1.record()
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) / steps * 1e3
-        out[name] = {"us": round(us, 1), "tflops": round(2.0 * M * N * K / us / 1e6, 1)}
+        out[name] = {"us": round(us, 1), "tflops": round(2.0 * M * N * K / us / 1e6, 1),
+                     "weight_tb_s": round(2.0 * N * K / us / 1e6, 2)}
         del a, w, c
     tot_us = sum(v["us"] for v in out.values())
-    tot_fl = sum(2.0 * M * N * K for N, K in ((qkv_n, H), (H, qd), (2 * F, H), (H, F)))
-    out["four_gemms"] = {"us": round(tot_us, 1), "mfma_frac": round(tot_fl / (tot_us * 1e-6) / PEAK_BF16, 4)}
+    shapes = ((qkv_n, H), (H, qd), (2 * F, H), (H, F))
+    tot_fl = sum(2.0 * M * N * K for N, K in shapes)
+    out["four_gemms"] = {"us": round(tot_us, 1), "mfma_frac": round(tot_fl / (tot_us * 1e-6) / PEAK_BF16, 4),
+                         "weight_tb_s": round(sum(2.0 * N * K for N, K in shapes) / tot_us / 1e6, 2)}
     return out
 
 
@@ -433,10 +436,13 @@ def gate_cells(hb, torch, dl, shape, steps, with_70b=True):
         gem = {k: v for k, v in kt.items() if k.startswith("gemm_")}
         g_s = sum(t for t, _, _ in gem.values())
         g_f = sum(f for _, f, _ in gem.values())
+        w_bytes = 2.0 * shp.hidden * ((shp.n_q_heads + 2 * shp.n_kv_heads) * shp.head_dim
+                                      + shp.n_q_heads * shp.head_dim + 3 * shp.ffn_dim)
         return {"layer_ms": round(sum(t for t, _, _ in kt.values()) * 1e3, 4),
                 "attention_ms": round(at_s * 1e3, 4), "attention_hbm_frac": round(at_b / at_s / PEAK_HBM, 4),
                 "attention_mfma_frac": round(at_f / at_s / PEAK_BF16, 4),
                 "gemms_ms": round(g_s * 1e3, 4), "gemms_mfma_frac": round(g_f / g_s / PEAK_BF16, 4),
+                "gemms_weight_tb_s": round(w_bytes / g_s / 1e12, 2),
                 "per_gemm_tflops": {k: round(f / t / 1e12, 1) for k, (t, f, _) in sorted(gem.items())}}
 
     out = {"decode_heavy": {}, "chunk_heavy": {}}
@@ -446,7 +452,8 @@ def gate_cells(hb, torch, dl, shape, steps, with_70b=True):
     for c in (1024, 2048):
         for n in (0, 32):
             out["chunk_heavy"][f"chunk {c} + {n} decodes"] = cell(dl, sweep_batch(c, n), shape)
-    out["blas_ceiling_8b_m2048"] = blas_ceiling(torch, shape, 2048)
+    for m in (256, 576, 2048):
+        out[f"blas_ceiling_8b_m{m}"] = blas_ceiling(torch, shape, m)
     if with_70b:
         b70 = llama70b_batch()
         l70 = DeviceRandomLayer(hb, torch, LLAMA3_70B, b70.num_blocks, b70.n_tokens, 64, 170)
@@ -756,8 +763,9 @@ def main() -> int:
         "cpu_baseline": cpu,
         "gates": gates,
         "gates_note": "per-kernel averages with every launch bracketed by events; algorithmic work as for roofline; "
-                      "GEMM times include their split-K reduces; blas_ceiling = torch.matmul on the same shapes "
-                      "without epilogues (context, not a target)",
+                      "GEMM times include their split-K reduces; gemms_weight_tb_s = the four GEMMs' weight bytes / "
+                      "their time; blas_ceiling = torch.matmul (hipBLASLt) on the same shapes without epilogues, one "
+                      "weight copy reused (context, not a target)",
         "latency_profile": profile,
         "latency_model": latency_model,
         "model_iteration": model,
