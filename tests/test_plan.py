@@ -138,3 +138,30 @@ def test_plan_merged_units_with_short_item_splits(driver):
     merged = [(-1 - u[0]) & ~(1 << 29) for u in plan["unit"] if u[0] < 0 and (-1 - u[0]) & (1 << 29)]
     assert any(it[5] == it[6] for v in merged for it in plan["item"][4 * v:4 * v + 4]), "no empty wave range"
     assert any(g[2] == 16 for g in plan["group"]), "no merge group of item workgroups"
+
+
+def test_plan_random_batches(driver):
+    """Seeded random batches (shape, CU count, request mix and forced item
+    split drawn per case): the coverage and slot invariants hold for every
+    plan, including merged units, empty wave ranges and merge groups."""
+    rng = np.random.default_rng(2503)
+    names = sorted(SHAPES)
+    for case in range(12):
+        name = names[rng.integers(len(names))]
+        cu = int(rng.choice([1, 4, 8, 64, 256]))
+        reqs, T = [], 0
+        for _ in range(int(rng.integers(1, 41))):
+            kind = rng.integers(3)
+            c = 1 if kind == 0 else int(rng.integers(2, 65)) if kind == 1 else int(rng.integers(65, 513))
+            if T + c > 1024:
+                break
+            reqs.append((c, int(rng.integers(0, 9000))))
+            T += c
+        if not reqs:
+            reqs = [(1, 100)]
+        split_item = int(rng.choice([0, 256, 512, 1024]))
+        plan = run_plan(driver, SHAPES[name], cu, reqs, split_item=split_item)
+        try:
+            check(plan, SHAPES[name], reqs)
+        except AssertionError as e:
+            raise AssertionError(f"case {case}: {name} cu={cu} split_item={split_item} reqs={reqs}: {e}") from e
