@@ -90,6 +90,38 @@ def test_small_shapes_parity(hb, monkeypatch, shape, splits):
     assert_parity(y, ref)
 
 
+
+@pytest.mark.parametrize("case", range(6))
+def test_random_batches_parity(hb, monkeypatch, case):
+    """Seeded random batches on the small shapes: decodes, short and long
+    chunks at random contexts, with the attention split lengths drawn too
+    (automatic, or forced short so that ranges spread over merged
+    workgroups, empty wave ranges and merge groups)."""
+    rng = np.random.default_rng(9100 + case)
+    shape = SMALL_SHAPES[case % len(SMALL_SHAPES)]
+    split_item = int(rng.choice([0, 256, 512]))
+    split_tile = int(rng.choice([0, 256, 1024]))
+    if split_item:
+        monkeypatch.setenv("HB_ATTN_SPLIT_ITEM", str(split_item))
+    if split_tile:
+        monkeypatch.setenv("HB_ATTN_SPLIT_TILE", str(split_tile))
+    lens, T = [], 0
+    for _ in range(int(rng.integers(4, 24))):
+        kind = rng.integers(3)
+        c = 1 if kind == 0 else int(rng.integers(2, 33)) if kind == 1 else int(rng.integers(33, 300))
+        if T + c > 600:
+            break
+        lens.append((c, int(rng.integers(0, 3000))))
+        T += c
+    b = make_batch(shape, lens, seed=9200 + case, num_blocks=4096)
+    print(f"case {case}: {shape.name} split_item={split_item} split_tile={split_tile} T={b.n_tokens} lens={lens}",
+          flush=True)
+    dl, w = _setup(hb, b)
+    y = _run(dl, b)
+    ref = oracle_for_batch(b, oracle.weights_to_f64(w))
+    print(shape.name, errors(y, ref))
+    assert_parity(y, ref)
+
 def _expected_slots(batch, which):
     """{(block, kv_head, slot): bits[hd]} of the prior context (which = 0 K, 1 V)."""
     out = {}
