@@ -88,6 +88,7 @@ struct AttnArgs {
   const uint16_t* k_pool;
   const uint16_t* v_pool;
   const int32_t* tiles;   // workgroup tiles (AttnItem)
+  int n_tiles;
   const int32_t* items;   // wave items (AttnItem)
   int n_items;
   const int32_t* units;   // per workgroup: tile index, or -1 - (group of 4 items)

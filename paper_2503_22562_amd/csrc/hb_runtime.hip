@@ -424,7 +424,7 @@ hb_status launch_layer(hb_layer* L, const hb_batch_desc* desc, const Prepared& p
   AttnArgs at{};
   at.q = L->q_rot; at.o = L->attn;
   at.k_pool = gq.k_pool; at.v_pool = gq.v_pool;
-  at.tiles = meta + p.off_tiles;
+  at.tiles = meta + p.off_tiles; at.n_tiles = p.n_tiles;
   at.items = meta + p.off_items; at.n_items = p.n_items;
   at.units = meta + p.off_units; at.n_units = p.n_units;
   at.groups = meta + p.off_groups; at.n_groups = p.n_groups;

@@ -14,7 +14,8 @@
 //
 // Two kinds of work share the launch, one per 256-thread workgroup (4 waves;
 // two workgroups per CU, so a compute-bound tile and a bandwidth-bound item
-// group can run side by side on one CU):
+// group can run side by side on one CU; one per CU when the launch holds no
+// tiles):
 //  * chunk tiles: 128 columns (4 waves x 32) of one request and kv head over a
 //    key range; 32-key K/V steps (two pool blocks) are copied as stored into
 //    a 4-stage LDS ring by global-to-LDS loads and every wave reads them from
@@ -721,16 +722,25 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   st16(a.o + (size_t)(gr.tok0 + pi) * a.nq * HD + h * HD + d, w);
 }
 
+// A launch without chunk tiles only streams K/V through wave items, and one
+// workgroup per CU does that faster than two (64 decodes of 512-4096 keys:
+// 109 -> 103 us; larger decode batches 0-1 % faster, none slower): such a
+// launch asks for more LDS than half a CU holds, so one workgroup fits per CU.
+// With tiles, two workgroups per CU (a tile beside a tile or an item group)
+// stay far faster.
+constexpr int kItemOnlyLds = 96 * 1024;
+
 template <int HD>
 void launch(hipStream_t s, const AttnArgs& a) {
   constexpr int lds = TSTAGES * TileGeom<HD>::STAGE;
+  static_assert(2 * lds <= 160 * 1024 && 2 * kItemOnlyLds > 160 * 1024 && kItemOnlyLds <= 160 * 1024, "occupancy");
   static bool attr = false;
   if (!attr) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<HD>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+                              hipFuncAttributeMaxDynamicSharedMemorySize, kItemOnlyLds);
     attr = true;
   }
-  attn_kernel<HD><<<a.n_units, 64 * WAVES, lds, s>>>(a);
+  attn_kernel<HD><<<a.n_units, 64 * WAVES, a.n_tiles > 0 ? lds : kItemOnlyLds, s>>>(a);
 }
 
 }  // namespace attn_detail

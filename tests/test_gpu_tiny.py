@@ -91,6 +91,23 @@ def test_small_shapes_parity(hb, monkeypatch, shape, splits):
 
 
 
+
+@pytest.mark.parametrize("shape", SMALL_SHAPES, ids=lambda s: s.name)
+def test_item_only_batches_parity(hb, shape):
+    """Batches without chunk tiles (decodes and chunks short enough to be wave
+    items), whose attention launch runs one workgroup per CU: decodes at
+    contexts from 0 to 5000, on block edges, one long enough to span several
+    merged workgroups, and a few short chunks."""
+    short = max(1, 64 // (shape.n_q_heads // shape.n_kv_heads) - 1)  # below the tile threshold
+    lens = [(1, 0), (1, 15), (1, 16), (1, 300), (1, 519), (1, 2000), (1, 3000), (1, 5000), (short, 40),
+            (short, 700), (2, 1), (1, 4097)]
+    b = make_batch(shape, lens, seed=78, num_blocks=1024)
+    dl, w = _setup(hb, b)
+    y = _run(dl, b)
+    ref = oracle_for_batch(b, oracle.weights_to_f64(w))
+    print(shape.name, "short chunk", short, errors(y, ref))
+    assert_parity(y, ref)
+
 @pytest.mark.parametrize("case", range(6))
 def test_random_batches_parity(hb, monkeypatch, case):
     """Seeded random batches on the small shapes: decodes, short and long
