@@ -4,9 +4,23 @@
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "hb_plan.h"
 
 namespace hb {
+
+// A launch with more than 64 KB of dynamic LDS needs the kernel's limit
+// raised first; HIP keeps that attribute per device, so it is raised once on
+// each device the kernel runs on (done: one bit per device ordinal).
+inline void raise_dynamic_lds(const void* kernel, int bytes, std::atomic<uint64_t>& done) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return;
+  const uint64_t bit = 1ull << dev;
+  if (done.load(std::memory_order_acquire) & bit) return;
+  if (hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess)
+    done.fetch_or(bit, std::memory_order_release);
+}
 
 // Per-token RoPE inputs for the QKV epilogue, written by the first RMSNorm:
 // cs[t][0..hd/2) = cos, cs[t][hd/2..hd) = sin of the angles pos(t) * inv_freq

@@ -734,12 +734,8 @@ template <int HD>
 void launch(hipStream_t s, const AttnArgs& a) {
   constexpr int lds = TSTAGES * TileGeom<HD>::STAGE;
   static_assert(2 * lds <= 160 * 1024 && 2 * kItemOnlyLds > 160 * 1024 && kItemOnlyLds <= 160 * 1024, "occupancy");
-  static bool attr = false;
-  if (!attr) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<HD>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, kItemOnlyLds);
-    attr = true;
-  }
+  static std::atomic<uint64_t> lds_raised{0};
+  raise_dynamic_lds(reinterpret_cast<const void*>(&attn_kernel<HD>), kItemOnlyLds, lds_raised);
   attn_kernel<HD><<<a.n_units, 64 * WAVES, a.n_tiles > 0 ? lds : kItemOnlyLds, s>>>(a);
 }
 

@@ -771,12 +771,8 @@ template <int TM, int TN, int WR, int WC, int ST, int EPI>
 void launch_tile(hipStream_t s, const GemmArgs& a, int tiles_m, int tiles_n, int ksplit, int kchunk, float* partial) {
   constexpr int lds = ST * 16 * (TM * WR + TN * WC) * 128;
   static_assert(lds <= 160 * 1024, "LDS");
-  static bool attr = false;
-  if (!attr) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_pipe_kernel<TM, TN, WR, WC, ST, EPI>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-    attr = true;
-  }
+  static std::atomic<uint64_t> lds_raised{0};
+  raise_dynamic_lds(reinterpret_cast<const void*>(&gemm_pipe_kernel<TM, TN, WR, WC, ST, EPI>), lds, lds_raised);
   gemm_pipe_kernel<TM, TN, WR, WC, ST, EPI>
       <<<tiles_m * tiles_n * ksplit, 64 * WR * WC, lds, s>>>(a, tiles_m, tiles_n, ksplit, kchunk, partial);
 }
