@@ -419,7 +419,7 @@ def blas_ceiling(torch, shape, M, steps=10):
     return out
 
 
-def gate_cells(hb, torch, dl, shape, steps, with_70b=True):
+def gate_cells(hb, torch, dl, shape, steps, with_70b=True, rates=None):
     """The fixed gate sets of the layer's targets: attention's HBM fraction on
     decode-heavy sweep cells (chunk 128/256 x 128/256 decodes), the four
     GEMMs' MFMA fraction on chunk-heavy cells (chunk 1024/2048 x 0/32 decodes)
@@ -443,7 +443,10 @@ def gate_cells(hb, torch, dl, shape, steps, with_70b=True):
                 "attention_mfma_frac": round(at_f / at_s / PEAK_BF16, 4),
                 "gemms_ms": round(g_s * 1e3, 4), "gemms_mfma_frac": round(g_f / g_s / PEAK_BF16, 4),
                 "gemms_weight_tb_s": round(w_bytes / g_s / 1e12, 2),
-                "per_gemm_tflops": {k: round(f / t / 1e12, 1) for k, (t, f, _) in sorted(gem.items())}}
+                "per_gemm_tflops": {k: round(f / t / 1e12, 1) for k, (t, f, _) in sorted(gem.items())},
+                **({"attention_frac_of_sustained_read": round(at_b / at_s / (rates["random_4kb_read_tb_s"] * 1e12), 4),
+                    "gemms_frac_of_sustained_mfma": round(g_f / g_s / (rates["mfma_bf16_pflop_s"] * 1e15), 4)}
+                   if rates else {})}
 
     out = {"decode_heavy": {}, "chunk_heavy": {}}
     for c in (128, 256):
@@ -466,6 +469,11 @@ def gate_cells(hb, torch, dl, shape, steps, with_70b=True):
     out["summary"] = {"decode_heavy_attention_hbm_frac_min": min(dh), "target_hbm": 0.60,
                       "chunk_heavy_gemms_mfma_frac_min": min(ch), "chunk_heavy_gemms_mfma_frac_max": max(ch),
                       "target_mfma": 0.50}
+    if rates:
+        out["summary"]["decode_heavy_attention_frac_of_sustained_read_min"] = min(
+            v["attention_frac_of_sustained_read"] for v in out["decode_heavy"].values())
+        out["summary"]["chunk_heavy_gemms_frac_of_sustained_mfma_min"] = min(
+            v["gemms_frac_of_sustained_mfma"] for v in out["chunk_heavy"].values())
     return out
 
 
@@ -537,6 +545,21 @@ def gpu_max_clock_mhz():
             except (IndexError, ValueError):
                 return None
     return None
+
+
+def device_rates(hb, torch, gib=8):
+    """Sustained rates of this GPU on fixed patterns (hb_measure_device_rates
+    over a gib-GiB region, about the paged pool's size): random 4-KB-chunk
+    reads (the paged-attention pattern), a streaming read, bf16 MFMAs on
+    varied operands. Context for the roofline fractions, whose denominators
+    stay the published peaks."""
+    buf = torch.empty(gib << 30, dtype=torch.uint8, device="cuda")
+    r = hb.hb_measure_device_rates(buf)
+    del buf
+    torch.cuda.empty_cache()
+    return {"random_4kb_read_tb_s": round(r["random_4kb_read_bytes_per_s"] / 1e12, 3),
+            "stream_read_tb_s": round(r["stream_read_bytes_per_s"] / 1e12, 3),
+            "mfma_bf16_pflop_s": round(r["mfma_bf16_flop_per_s"] / 1e15, 3), "region_gib": gib}
 
 
 def device_info(torch):
@@ -681,6 +704,14 @@ def main() -> int:
     roof["algorithmic_bytes"] = by
     tr = measured_traffic(dom, "llama3-8b")
     roof["traffic"] = tr
+    log("bench: device rates (random 4-KB reads, streaming read, MFMA loop)")
+    rates = device_rates(hb, torch)
+    sus = rates["mfma_bf16_pflop_s"] * 1e3 if roof["bound"] == "mfma" else rates["random_4kb_read_tb_s"] * 1e3
+    roof["sustained_peak"] = round(sus, 1)
+    roof["frac_of_sustained"] = round(roof["achieved"] / sus, 4) if sus > 0 else None
+    roof["sustained_note"] = ("sustained_peak: this GPU's rate measured in this run on the kernel's pattern "
+                              "(bf16 MFMA loop on varied operands, or random 4-KB reads for an HBM-bound "
+                              "kernel; device.rates); context only, frac uses the published peak")
     flops, bytes_ = layer_work(shape, [(c, xx) for c, xx, _ in reqs])
     step_s = ms_per_step * 1e-3
 
@@ -689,7 +720,7 @@ def main() -> int:
     gates = None
     if not a.no_regimes:
         log("bench: gate cells (decode-heavy and chunk-heavy sweep cells, 70B layer, hipBLASLt ceiling)")
-        gates = gate_cells(hb, torch, dl, shape, a.regime_steps)
+        gates = gate_cells(hb, torch, dl, shape, a.regime_steps, rates=rates)
 
     profile = None
     if not a.no_profile:
@@ -769,7 +800,7 @@ def main() -> int:
         "latency_profile": profile,
         "latency_model": latency_model,
         "model_iteration": model,
-        "device": device_info(torch),
+        "device": dict(device_info(torch), rates=rates),
     }
     print(json.dumps(out), flush=True)
     return 0

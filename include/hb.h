@@ -404,6 +404,29 @@ hb_status hb_plan_gemms(const hb_layer_config* cfg, int32_t n_tokens, int32_t cu
  * Errors: HB_ERR_INVALID (null pointer). */
 hb_status hb_layer_gemm_plans(hb_layer* layer, int32_t* tile, int32_t* ksplit);
 
+/* Sustained rates of the current device on three fixed access patterns,
+ * measured for reading the kernels' roofline fractions against what the
+ * device delivers (the published peaks remain the denominators of record):
+ *   random_4kb_read_bytes_per_s  waves reading random 4-KB chunks of the first
+ *                                min(bytes, 8 GiB) of buf (the pool-block pattern
+ *                                of paged attention; the rate depends on the region
+ *                                size), 2048 workgroups x 4 waves x 32 chunks;
+ *   stream_read_bytes_per_s      a sequential grid-stride read of that region;
+ *   mfma_bf16_flop_per_s         16x16x32 bf16 MFMAs on pseudo-random operands held
+ *                                in registers, two 4-wave workgroups per CU (varied
+ *                                data draws more power than constant operands).
+ * Each is the best of three timed launches on `stream` (hipStream_t, 0 = the
+ * null stream); the call waits for them. buf: device memory of `bytes` bytes,
+ * at least 1 GiB so that the reads exceed the last-level cache, whose contents
+ * are overwritten only in a case that does not occur in practice (treat it as
+ * scratch). Errors: HB_ERR_INVALID (null pointer, bytes < 1 GiB), HB_ERR_HIP. */
+typedef struct {
+  double random_4kb_read_bytes_per_s;
+  double stream_read_bytes_per_s;
+  double mfma_bf16_flop_per_s;
+} hb_device_rates;
+hb_status hb_measure_device_rates(void* buf, int64_t bytes, void* stream, hb_device_rates* out);
+
 /* Message for the last non-OK status returned on this host thread. */
 const char* hb_last_error(void);
 

@@ -18,7 +18,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhb.so")
 ARCH = "gfx950"
 
-SOURCES = ["hb_plan.cpp", "hb_predict.cpp", "hb_runtime.hip", "hb_model.hip", "k_elementwise.hip", "k_gemm.hip", "k_attention.hip"]
+SOURCES = ["hb_plan.cpp", "hb_predict.cpp", "hb_runtime.hip", "hb_model.hip", "k_elementwise.hip", "k_gemm.hip", "k_attention.hip", "k_probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["-O3", "-fPIC", "-std=c++17", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]

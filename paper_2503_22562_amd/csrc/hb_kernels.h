@@ -128,6 +128,15 @@ void launch_fill_blocks(hipStream_t s, const int32_t* blocks, int n, int nkv, in
                         uint16_t* v_pool, uint64_t seed);
 // Overwrite a buffer (evicts earlier data from the Infinity Cache).
 void launch_flush(hipStream_t s, void* buf, int64_t bytes, uint32_t value);
+
+// Sustained-rate probes (k_probe.hip): waves reading random 4-KB chunks of
+// buf[0, 4096 n_chunks), a grid-stride read of buf[0, bytes), and a loop of
+// bf16 MFMAs (blocks x 4 waves x iters x 16 of them). sink: a device word the
+// kernels write only in a case that does not occur in practice.
+void launch_probe_random_read(hipStream_t s, const void* buf, uint32_t n_chunks, int blocks, int iters,
+                              uint32_t* sink);
+void launch_probe_stream_read(hipStream_t s, const void* buf, int64_t bytes, int blocks, uint32_t* sink);
+void launch_probe_mfma(hipStream_t s, int blocks, int iters, uint32_t* sink);
 // out[r][:] = src[clamp(rows[r], 0, n_src - 1)][:] (bf16 rows of H, H % 8 == 0).
 void launch_gather_rows(hipStream_t s, const uint16_t* src, int64_t n_src, const int32_t* rows, int n_rows, int H,
                         uint16_t* out);

@@ -798,6 +798,60 @@ hb_status hb_layer_gemm_plans(hb_layer* L, int32_t* tile, int32_t* ksplit) {
   return HB_OK;
 }
 
+namespace {
+// Two events, destroyed with the scope.
+struct EventPair {
+  hipEvent_t a = nullptr, b = nullptr;
+  ~EventPair() {
+    if (a) (void)hipEventDestroy(a);
+    if (b) (void)hipEventDestroy(b);
+  }
+};
+}  // namespace
+
+hb_status hb_measure_device_rates(void* buf, int64_t bytes, void* stream, hb_device_rates* out) {
+  if (!buf || !out || bytes < ((int64_t)1 << 30))
+    return fail(HB_ERR_INVALID, "hb_measure_device_rates: null pointer or a buffer below 1 GiB (%lld bytes)",
+                (long long)bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int dev = 0, cus = 0;
+  HB_HIP(hipGetDevice(&dev));
+  HB_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  cus = std::max(1, cus);
+  const int64_t region = std::min<int64_t>(bytes, (int64_t)8 << 30) & ~(int64_t)4095;
+  uint32_t* sink = static_cast<uint32_t*>(buf);
+  EventPair ev;
+  HB_HIP(hipEventCreate(&ev.a));
+  HB_HIP(hipEventCreate(&ev.b));
+  // best of three timed launches (ms)
+  auto best_ms = [&](auto&& launch, float* ms) -> hipError_t {
+    *ms = 0.f;
+    for (int r = 0; r < 3; ++r) {
+      hipError_t e = hipEventRecord(ev.a, s);
+      if (e == hipSuccess) { launch(); e = hipGetLastError(); }
+      if (e == hipSuccess) e = hipEventRecord(ev.b, s);
+      if (e == hipSuccess) e = hipEventSynchronize(ev.b);
+      float t = 0.f;
+      if (e == hipSuccess) e = hipEventElapsedTime(&t, ev.a, ev.b);
+      if (e != hipSuccess) return e;
+      if (r == 0 || t < *ms) *ms = t;
+    }
+    return hipSuccess;
+  };
+  constexpr int kReadWgs = 2048, kChunksPerWave = 32, kMfmaIters = 4096;
+  float ms_rand = 0.f, ms_stream = 0.f, ms_mfma = 0.f;
+  HB_HIP(best_ms([&] { launch_probe_random_read(s, buf, (uint32_t)(region / 4096), kReadWgs, kChunksPerWave, sink); },
+                 &ms_rand));
+  HB_HIP(best_ms([&] { launch_probe_stream_read(s, buf, region, 8 * cus, sink); }, &ms_stream));
+  HB_HIP(best_ms([&] { launch_probe_mfma(s, 2 * cus, kMfmaIters, sink); }, &ms_mfma));
+  const double rand_bytes = (double)kReadWgs * 4 * kChunksPerWave * 4096;
+  const double mfma_flops = (double)(2 * cus) * 4 * kMfmaIters * 16 * (2.0 * 16 * 16 * 32);
+  out->random_4kb_read_bytes_per_s = ms_rand > 0.f ? rand_bytes / (ms_rand * 1e-3) : 0.0;
+  out->stream_read_bytes_per_s = ms_stream > 0.f ? (double)region / (ms_stream * 1e-3) : 0.0;
+  out->mfma_bf16_flop_per_s = ms_mfma > 0.f ? mfma_flops / (ms_mfma * 1e-3) : 0.0;
+  return HB_OK;
+}
+
 hb_status hb_layer_stage(hb_layer* L, int32_t stage, void** dev_ptr, int64_t* row_stride) {
   if (!L || !dev_ptr || !row_stride) return fail(HB_ERR_INVALID, "null argument");
   switch (stage) {

@@ -25,7 +25,8 @@ EXPORTED = ("hb_create_layer", "hb_destroy_layer", "hb_append_kv", "hb_run_itera
             "hb_profile", "hb_profile_batches", "hb_latency_features", "hb_fit_latency_model", "hb_predict_latency", "hb_select_chunk",
             "hb_create_model", "hb_destroy_model", "hb_model_layer", "hb_run_model",
             "hb_set_kernel_timing", "hb_kernel_times", "hb_kernel_name", "hb_layer_stage", "hb_last_error",
-            "hb_gemm_tile_count", "hb_plan_gemms", "hb_layer_gemm_plans", "hb_run_iteration_noalloc")
+            "hb_gemm_tile_count", "hb_plan_gemms", "hb_layer_gemm_plans", "hb_run_iteration_noalloc",
+            "hb_measure_device_rates")
 HB_LAT_FEATURES = 5
 
 
@@ -52,6 +53,11 @@ class hb_request(C.Structure):
 class hb_batch_desc(C.Structure):
     _fields_ = [("n_requests", C.c_int32), ("requests", C.POINTER(hb_request)),
                 ("x_in", C.c_void_p), ("x_out", C.c_void_p), ("out_dtype", C.c_int32)]
+
+
+class hb_device_rates(C.Structure):
+    _fields_ = [("random_4kb_read_bytes_per_s", C.c_double), ("stream_read_bytes_per_s", C.c_double),
+                ("mfma_bf16_flop_per_s", C.c_double)]
 
 
 class hb_decode_mix(C.Structure):
@@ -159,6 +165,8 @@ def load() -> C.CDLL:
     lib.hb_plan_gemms.restype = st
     lib.hb_layer_gemm_plans.argtypes = [C.c_void_p, C.POINTER(C.c_int32), C.POINTER(C.c_int32)]
     lib.hb_layer_gemm_plans.restype = st
+    lib.hb_measure_device_rates.argtypes = [C.c_void_p, C.c_int64, C.c_void_p, C.POINTER(hb_device_rates)]
+    lib.hb_measure_device_rates.restype = st
     _lib = lib
     return lib
 
@@ -496,3 +504,13 @@ def hb_layer_stage(layer: Layer, stage: int) -> Tuple[int, int]:
     s = C.c_int64()
     _check(load().hb_layer_stage(layer.handle, int(stage), C.byref(p), C.byref(s)))
     return int(p.value or 0), int(s.value)
+
+
+def hb_measure_device_rates(buf, stream=None) -> Dict[str, float]:
+    """Sustained random-4-KB read, streaming read and bf16 MFMA rates of the
+    current device; buf: a device tensor of at least 1 GiB (scratch)."""
+    r = hb_device_rates()
+    s = 0 if stream is None else int(stream.cuda_stream)
+    _check(load().hb_measure_device_rates(C.c_void_p(buf.data_ptr()), int(buf.numel() * buf.element_size()),
+                                          C.c_void_p(s), C.byref(r)))
+    return {f[0]: float(getattr(r, f[0])) for f in hb_device_rates._fields_}

@@ -223,3 +223,15 @@ def test_pool_layout_views(hd):
             v[:, :, s // 8, d, s % 8] = want[:, :, s, d]
     assert np.array_equal(k_by_slot(k.reshape(nb, nkv, 16, hd)), want)
     assert np.array_equal(v_by_slot(v), want)
+
+
+def test_device_rates_argument_errors(H):
+    """hb_measure_device_rates rejects a null buffer or output and a buffer
+    below 1 GiB before touching a device."""
+    import ctypes as C
+    out = H.hb_device_rates()
+    lib = H.load()
+    assert lib.hb_measure_device_rates(None, 1 << 30, None, C.byref(out)) == H.HB_ERR_INVALID
+    assert lib.hb_measure_device_rates(C.c_void_p(4096), (1 << 30) - 1, None, C.byref(out)) == H.HB_ERR_INVALID
+    assert lib.hb_measure_device_rates(C.c_void_p(4096), 1 << 30, None, None) == H.HB_ERR_INVALID
+    assert "1 GiB" in H.hb_last_error()

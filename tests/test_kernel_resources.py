@@ -1,4 +1,4 @@
-"""Register budgets of the GEMM and elementwise kernels (CPU, hipcc only): no
+"""Register budgets of the GEMM, elementwise and probe kernels (CPU, hipcc only): no
 instantiation spills VGPRs. A spill in an 8-wave GEMM tile lands in its K loop
 (scratch traffic on every stage); the residual-epilogue instantiations once
 spilled 40-103 registers that way."""
@@ -15,7 +15,7 @@ sys.path.insert(0, ROOT)
 
 
 @pytest.mark.skipif(not os.path.exists("/opt/rocm/bin/hipcc") and shutil.which("hipcc") is None, reason="no hipcc")
-@pytest.mark.parametrize("src", ["k_gemm.hip", "k_elementwise.hip"])
+@pytest.mark.parametrize("src", ["k_gemm.hip", "k_elementwise.hip", "k_probe.hip"])
 def test_no_vgpr_spills(src, tmp_path):
     from paper_2503_22562_amd import build as B
     cmd = [B.HIPCC, *B.COMMON, *B.HIP_FLAGS, *B.EXTRA_FLAGS.get(src, []), "--cuda-device-only",
