@@ -162,8 +162,9 @@ static void launch_gemm_regstaged(hipStream_t s, const GemmArgs& a) {
 // ---------------------------------------------------------------------------
 // LDS-pipelined GEMM for K % 64 == 0.
 //
-// Tile BM x BN = 32 TM x 32 TN; 4 waves in a 2 x 2 arrangement each own a
-// 16 TM x 16 TN block of 16x16 MFMA tiles (accumulators in AGPRs). K advances
+// Tile BM x BN = 16 TM WR x 16 TN WC: WR x WC waves (2 x 2, 2 x 4 or 4 x 2)
+// each own TM x TN 16x16 MFMA blocks (accumulators in VGPRs: the kernels are
+// built with the MFMA VGPR form, so no copies between register files). K advances
 // in stages of 64 through a ring of S LDS buffers that global memory fills
 // directly (16-byte global-to-LDS loads, no register staging). A 1-KB load
 // instruction of a wave fills eight 128-byte rows; inside a row the eight
