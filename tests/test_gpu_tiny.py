@@ -265,6 +265,19 @@ def test_edge_cases_positions_and_capacity(hb):
     assert_parity(y, ref)
 
 
+
+def test_long_contexts_parity(hb):
+    """Contexts of 64K-131K tokens: decodes whose key ranges spread over many
+    merged workgroups and merge parts, and a chunk whose tiles are cut into
+    ~25 key splits combined by the merge kernel."""
+    lens = [(1, 131072), (64, 100000), (1, 65535), (1, 98304)]
+    b = make_batch(TINY, lens, seed=14, num_blocks=26000)
+    dl, w = _setup(hb, b)
+    y = _run(dl, b)
+    ref = oracle_for_batch(b, oracle.weights_to_f64(w))
+    print("long contexts", errors(y, ref))
+    assert_parity(y, ref)
+
 def test_empty_batch_is_noop_and_errors_touch_nothing(hb):
     import torch
     from paper_2503_22562_amd import hb as H
