@@ -278,6 +278,25 @@ def test_long_contexts_parity(hb):
     print("long contexts", errors(y, ref))
     assert_parity(y, ref)
 
+
+def test_shared_prefix_blocks_parity(hb):
+    """Requests that share read-only prefix blocks (prefix caching): three
+    requests read the same two cached blocks (positions 0-31) and write their
+    new tokens into blocks of their own; a fourth shares one block with the
+    first and diverges after it. The cached values of a shared block are the
+    last writer's on both sides (prior context is seeded in request order)."""
+    lens = [(1, 40), (1, 40), (8, 32), (3, 20)]
+    b = make_batch(TINY, lens, seed=15, num_blocks=64)
+    b.requests[0].block_table = np.array([5, 9, 2], np.int32)
+    b.requests[1].block_table = np.array([5, 9, 3], np.int32)
+    b.requests[2].block_table = np.array([5, 9, 4], np.int32)
+    b.requests[3].block_table = np.array([5, 7], np.int32)
+    dl, w = _setup(hb, b)
+    y = _run(dl, b)
+    ref = oracle_for_batch(b, oracle.weights_to_f64(w))
+    print("shared prefix", errors(y, ref))
+    assert_parity(y, ref)
+
 def test_empty_batch_is_noop_and_errors_touch_nothing(hb):
     import torch
     from paper_2503_22562_amd import hb as H
