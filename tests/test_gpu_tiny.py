@@ -297,6 +297,19 @@ def test_shared_prefix_blocks_parity(hb):
     print("shared prefix", errors(y, ref))
     assert_parity(y, ref)
 
+
+def test_many_requests_parity(hb):
+    """400 decodes at contexts 0-600 and two chunks in one batch (metadata of
+    hundreds of requests, hundreds of item groups, tiles beside them)."""
+    rng = np.random.default_rng(16)
+    lens = [(1, int(c)) for c in rng.integers(0, 600, 400)] + [(40, 300), (33, 0)]
+    b = make_batch(TINY, lens, seed=16, num_blocks=16384)
+    dl, w = _setup(hb, b)
+    y = _run(dl, b)
+    ref = oracle_for_batch(b, oracle.weights_to_f64(w))
+    print("many requests", errors(y, ref))
+    assert_parity(y, ref)
+
 def test_empty_batch_is_noop_and_errors_touch_nothing(hb):
     import torch
     from paper_2503_22562_amd import hb as H
