@@ -310,6 +310,28 @@ def test_many_requests_parity(hb):
     print("many requests", errors(y, ref))
     assert_parity(y, ref)
 
+
+def test_layer_on_a_side_stream(hb):
+    """A layer created while a non-default stream is current enqueues its work
+    there: inputs written and outputs read on that stream give the oracle's
+    result, for both entry points."""
+    import torch
+    from paper_2503_22562_amd import hb as H
+    from paper_2503_22562_amd.harness import to_device_bf16
+    b = tiny_batch()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        dl, w = _setup(hb, b)
+        x = to_device_bf16(b.x_in())
+        y = dl.run(_reqs(b), x)
+        y2 = torch.empty_like(y)
+        H.hb_run_iteration_noalloc(dl.layer, _reqs(b), x, y2)
+        side.synchronize()
+        got, got2 = y.cpu().numpy().astype(np.float64), y2.cpu().numpy().astype(np.float64)
+    ref = oracle_for_batch(b, oracle.weights_to_f64(w))
+    assert_parity(got, ref)
+    assert np.array_equal(got, got2)
+
 def test_empty_batch_is_noop_and_errors_touch_nothing(hb):
     import torch
     from paper_2503_22562_amd import hb as H
