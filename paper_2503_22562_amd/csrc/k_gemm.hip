@@ -288,6 +288,14 @@ __device__ __forceinline__ void interleave_loads_reads() {
   if (NMFMA > slots) __builtin_amdgcn_sched_group_barrier(0x008, NMFMA > slots ? NMFMA - slots : 1, 0);
 }
 
+// Whether a tile (TM x TN blocks per wave, NW waves) applies RoPE in its own
+// epilogue for head size hd: each wave row must span whole heads (rotation
+// partners in one lane), and 8-wave tiles (256 VGPRs per wave) must keep
+// their accumulators within 128 VGPRs to leave room for the rotation.
+constexpr bool rope_in_tile(int tm, int tn, int nw, int hd) {
+  return (16 * tn) % hd == 0 && (nw == 4 || tm * tn <= 32);
+}
+
 // QKV epilogue of one accumulator row (TN fragments of 4 columns, starting at
 // a head boundary nbase): q and k heads are rotated pairwise (column j with
 // j + hd/2, PAIR = hd/32 fragments apart, both in this lane) with the row's
@@ -537,8 +545,14 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_pipe_kernel(GemmArgs a, int
       continue;
     }
     if (EPI == GEMM_QKV_ROPE) {
-      if (a.hd == 128) qkv_rope_row<TN, 4>(a, acc[mi], m, nt * BN + wn * WN, cq);
-      else qkv_rope_row<TN, 2>(a, acc[mi], m, nt * BN + wn * WN, cq);
+      // the planner sends tiles that cannot rotate in-tile (rope_in_tile)
+      // through a K split, so their rows are not built
+      if constexpr (rope_in_tile(TM, TN, NW, 128)) {
+        if (a.hd == 128) qkv_rope_row<TN, 4>(a, acc[mi], m, nt * BN + wn * WN, cq);
+        else qkv_rope_row<TN, 2>(a, acc[mi], m, nt * BN + wn * WN, cq);
+      } else if constexpr (rope_in_tile(TM, TN, NW, 64)) {
+        if (a.hd == 64) qkv_rope_row<TN, 2>(a, acc[mi], m, nt * BN + wn * WN, cq);
+      }
       continue;
     }
     if (EPI == GEMM_SWIGLU) {
@@ -765,6 +779,7 @@ constexpr TileCfg kTiles[] = {
     {6, 4, 2, 4, 2, 1.411f, 1.411f, 1.188f, 7.69f},  {4, 4, 2, 4, 3, 0.999f, 0.999f, 0.863f, 2.13f},
     {4, 8, 4, 2, 2, 1.512f, 1.512f, 1.305f, 10.75f}, {3, 8, 4, 2, 2, 1.427f, 1.427f, 1.235f, 5.37f},
     {2, 8, 4, 2, 3, 1.000f, 1.000f, 0.857f, 4.33f},  {6, 6, 2, 4, 2, 1.636f, 1.636f, 1.499f, 12.96f},
+    {9, 4, 2, 4, 2, 1.546f, 1.546f, 1.417f, 12.96f},
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 
@@ -794,7 +809,8 @@ void launch_cfg(int idx, hipStream_t s, const GemmArgs& a, int tm, int tn, int k
     case 10: launch_tile<4, 8, 4, 2, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
     case 11: launch_tile<3, 8, 4, 2, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
     case 12: launch_tile<2, 8, 4, 2, 3, EPI>(s, a, tm, tn, ks, kchunk, part); break;
-    default: launch_tile<6, 6, 2, 4, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    case 13: launch_tile<6, 6, 2, 4, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
+    default: launch_tile<9, 4, 2, 4, 2, EPI>(s, a, tm, tn, ks, kchunk, part); break;
   }
 }
 
@@ -863,9 +879,11 @@ static GemmPlan search_plan(const GemmArgs& a, int cu_count, int force_cfg, int 
   GemmPlan best{-1, 0, 0, 1, 0};
   double best_cost = 1e300;
   const int ksteps = a.K / 64;
-  // the in-tile QKV epilogue needs whole heads in a wave (rotation partners in
-  // one lane); with a K split the reduce kernel rotates, and any tile fits
-  auto fits = [&](const TileCfg& c, int ks) { return a.epi != GEMM_QKV_ROPE || ks > 1 || (16 * c.tn) % a.hd == 0; };
+  // tiles that cannot rotate in their epilogue take QKV with a K split, whose
+  // reduce kernel rotates
+  auto fits = [&](const TileCfg& c, int ks) {
+    return a.epi != GEMM_QKV_ROPE || ks > 1 || rope_in_tile(c.tm, c.tn, c.wr * c.wc, a.hd);
+  };
   const int W = partial_width(a);
   for (int i = 0; i < kNumTiles; ++i) {
     if (force_cfg >= 0 && i != force_cfg) continue;

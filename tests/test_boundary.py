@@ -195,7 +195,8 @@ def test_gemm_plans_host_only(H):
     from hb_workloads import LLAMA3_8B
     cfg = H.make_config(LLAMA3_8B, 4096, 512)
     n = H.hb_gemm_tile_count()
-    assert n >= 1
+    from test_gpu_tiny import GEMM_TILE_SHAPES
+    assert n == GEMM_TILE_SHAPES  # the forced-tile GPU test runs every shape
     for T in (1, 64, 128, 576, 2048, 4096):
         for tile, ks in H.hb_plan_gemms(cfg, T, 256):
             assert 0 <= tile < n and 1 <= ks <= 8

@@ -58,6 +58,10 @@ def test_tiny_parity_all_rows_and_stages(hb):
     assert_swiglu_stage(m, st, w64, b.shape.rms_eps)
 
 
+# LDS-pipelined GEMM tile shapes of the library (hb_gemm_tile_count; a CPU test
+# keeps the two equal)
+GEMM_TILE_SHAPES = 15
+
 SMALL_SHAPES = [
     LayerShape("g8-hd64", 512, 8, 1, 64, 256, weight_seed=11),
     LayerShape("g1-hd128", 512, 4, 4, 128, 336, weight_seed=12),
@@ -372,7 +376,7 @@ def test_bf16_output_matches_fp32_output(hb):
     assert torch.equal(y16, ref)
 
 
-@pytest.mark.parametrize("tile", list(range(14)))
+@pytest.mark.parametrize("tile", list(range(GEMM_TILE_SHAPES)))
 @pytest.mark.parametrize("ksplit", [1, 2, 3])
 def test_every_gemm_tile_shape(hb, monkeypatch, tile, ksplit):
     """Each LDS-pipelined GEMM tile shape, whole K or split (the split-K
