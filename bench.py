@@ -13,6 +13,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import subprocess
@@ -80,10 +81,16 @@ def layer_work(shape, requests, out_f32=True):
 
 
 def kernel_sources_digest(names):
+    """Digest of the code of the given sources: comments and whitespace are
+    dropped, so that only a change to the code itself invalidates counters
+    taken from it."""
     h = hashlib.sha256()
     for n in names:
-        with open(os.path.join(ROOT, "paper_2503_22562_amd", "csrc", n), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2503_22562_amd", "csrc", n)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
