@@ -15,7 +15,11 @@ namespace hb {
 // each device the kernel runs on (done: one bit per device ordinal).
 inline void raise_dynamic_lds(const void* kernel, int bytes, std::atomic<uint64_t>& done) {
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return;
+  if (dev >= 64) {  // beyond the bit set: raise it on every call
+    (void)hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    return;
+  }
   const uint64_t bit = 1ull << dev;
   if (done.load(std::memory_order_acquire) & bit) return;
   if (hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess)
