@@ -426,6 +426,31 @@ def blas_ceiling(torch, shape, M, steps=10):
     return out
 
 
+def regime_cell(hb, torch, layer, b, shp, steps, rates=None):
+    """One batch on a layer, every launch bracketed by events: attention's
+    HBM and MFMA fractions, the four GEMMs' MFMA fraction (split-K reduces
+    included) and weight rate, per-GEMM TFLOP/s."""
+    from paper_2503_22562_amd.harness import to_device_bf16
+    x = to_device_bf16(b.x_in())
+    y = torch.empty((b.n_tokens, shp.hidden), dtype=torch.float32, device="cuda")
+    kt = regime(hb, layer, b, shp, x, y, steps)
+    at_s, at_f, at_b = kt["attention"]
+    gem = {k: v for k, v in kt.items() if k.startswith("gemm_")}
+    g_s = sum(t for t, _, _ in gem.values())
+    g_f = sum(f for _, f, _ in gem.values())
+    w_bytes = 2.0 * shp.hidden * ((shp.n_q_heads + 2 * shp.n_kv_heads) * shp.head_dim
+                                  + shp.n_q_heads * shp.head_dim + 3 * shp.ffn_dim)
+    return {"layer_ms": round(sum(t for t, _, _ in kt.values()) * 1e3, 4),
+            "attention_ms": round(at_s * 1e3, 4), "attention_hbm_frac": round(at_b / at_s / PEAK_HBM, 4),
+            "attention_mfma_frac": round(at_f / at_s / PEAK_BF16, 4),
+            "gemms_ms": round(g_s * 1e3, 4), "gemms_mfma_frac": round(g_f / g_s / PEAK_BF16, 4),
+            "gemms_weight_tb_s": round(w_bytes / g_s / 1e12, 2),
+            "per_gemm_tflops": {k: round(f / t / 1e12, 1) for k, (t, f, _) in sorted(gem.items())},
+            **({"attention_frac_of_sustained_read": round(at_b / at_s / (rates["random_4kb_read_tb_s"] * 1e12), 4),
+                "gemms_frac_of_sustained_mfma": round(g_f / g_s / (rates["mfma_bf16_pflop_s"] * 1e15), 4)}
+               if rates else {})}
+
+
 def gate_cells(hb, torch, dl, shape, steps, with_70b=True, rates=None):
     """The fixed gate sets of the layer's targets: attention's HBM fraction on
     decode-heavy sweep cells (chunk 128/256 x 128/256 decodes), the four
@@ -433,27 +458,9 @@ def gate_cells(hb, torch, dl, shape, steps, with_70b=True, rates=None):
     and on the 70B layer (chunk 2048 at 30720 + 32 decodes at 32768); with
     hipBLASLt on the same GEMM shapes as context."""
     from hb_workloads import LLAMA3_70B, llama70b_batch, sweep_batch
-    from paper_2503_22562_amd.harness import to_device_bf16
 
     def cell(layer, b, shp):
-        x = to_device_bf16(b.x_in())
-        y = torch.empty((b.n_tokens, shp.hidden), dtype=torch.float32, device="cuda")
-        kt = regime(hb, layer, b, shp, x, y, steps)
-        at_s, at_f, at_b = kt["attention"]
-        gem = {k: v for k, v in kt.items() if k.startswith("gemm_")}
-        g_s = sum(t for t, _, _ in gem.values())
-        g_f = sum(f for _, f, _ in gem.values())
-        w_bytes = 2.0 * shp.hidden * ((shp.n_q_heads + 2 * shp.n_kv_heads) * shp.head_dim
-                                      + shp.n_q_heads * shp.head_dim + 3 * shp.ffn_dim)
-        return {"layer_ms": round(sum(t for t, _, _ in kt.values()) * 1e3, 4),
-                "attention_ms": round(at_s * 1e3, 4), "attention_hbm_frac": round(at_b / at_s / PEAK_HBM, 4),
-                "attention_mfma_frac": round(at_f / at_s / PEAK_BF16, 4),
-                "gemms_ms": round(g_s * 1e3, 4), "gemms_mfma_frac": round(g_f / g_s / PEAK_BF16, 4),
-                "gemms_weight_tb_s": round(w_bytes / g_s / 1e12, 2),
-                "per_gemm_tflops": {k: round(f / t / 1e12, 1) for k, (t, f, _) in sorted(gem.items())},
-                **({"attention_frac_of_sustained_read": round(at_b / at_s / (rates["random_4kb_read_tb_s"] * 1e12), 4),
-                    "gemms_frac_of_sustained_mfma": round(g_f / g_s / (rates["mfma_bf16_pflop_s"] * 1e15), 4)}
-                   if rates else {})}
+        return regime_cell(hb, torch, layer, b, shp, steps, rates)
 
     out = {"decode_heavy": {}, "chunk_heavy": {}}
     for c in (128, 256):
@@ -481,6 +488,29 @@ def gate_cells(hb, torch, dl, shape, steps, with_70b=True, rates=None):
             v["attention_frac_of_sustained_read"] for v in out["decode_heavy"].values())
         out["summary"]["chunk_heavy_gemms_frac_of_sustained_mfma_min"] = min(
             v["gemms_frac_of_sustained_mfma"] for v in out["chunk_heavy"].values())
+    return out
+
+
+def tp_shard_cells(hb, torch, steps, rates=None):
+    """One GPU's share of a layer under tensor parallelism, sharded by heads
+    (the 8B layer at TP2 on the bench batch's request mix, the 70B layer at
+    TP8 on the 70B mix): the shard's kernels at their real shapes, timed like
+    the gate cells. The two all-reduces of the [T, hidden] activations per
+    layer that tensor parallelism adds are not run on one GPU; their bf16
+    payload is reported."""
+    from hb_workloads import LLAMA3_8B_TP2, LLAMA3_70B_TP8, llama70b_batch, llama8b_batch
+    out = {}
+    for shp, b in ((LLAMA3_8B_TP2, llama8b_batch(shape=LLAMA3_8B_TP2)),
+                   (LLAMA3_70B_TP8, llama70b_batch(shape=LLAMA3_70B_TP8))):
+        layer = DeviceRandomLayer(hb, torch, shp, b.num_blocks, b.n_tokens, len(b.requests), shp.weight_seed)
+        c = regime_cell(hb, torch, layer, b, shp, steps, rates)
+        c["shape"] = {"hidden": shp.hidden, "n_q_heads": shp.n_q_heads, "n_kv_heads": shp.n_kv_heads,
+                      "head_dim": shp.head_dim, "ffn_dim": shp.ffn_dim}
+        c["tokens"] = b.n_tokens
+        c["allreduce_bytes_per_layer"] = 2 * b.n_tokens * shp.hidden * 2
+        out[b.label] = c
+        del layer
+        torch.cuda.empty_cache()
     return out
 
 
@@ -724,10 +754,12 @@ def main() -> int:
 
     # the gate cells of the layer's targets (decode-heavy: attention's HBM
     # rate; chunk-heavy: the GEMMs' MFMA rate), hipBLASLt as context
-    gates = None
+    gates = shards = None
     if not a.no_regimes:
         log("bench: gate cells (decode-heavy and chunk-heavy sweep cells, 70B layer, hipBLASLt ceiling)")
         gates = gate_cells(hb, torch, dl, shape, a.regime_steps, rates=rates)
+        log("bench: tensor-parallel shards (8B at TP2, 70B at TP8)")
+        shards = tp_shard_cells(hb, torch, a.regime_steps, rates=rates)
 
     profile = None
     if not a.no_profile:
@@ -804,6 +836,11 @@ def main() -> int:
                       "GEMM times include their split-K reduces; gemms_weight_tb_s = the four GEMMs' weight bytes / "
                       "their time; blas_ceiling = torch.matmul (hipBLASLt) on the same shapes without epilogues, one "
                       "weight copy reused (context, not a target)",
+        "tp_shards": shards,
+        "tp_shards_note": "one GPU's share of a layer sharded by heads (QKV and gate/up by output columns, O and "
+                          "down by input columns, pool and attention by kv head), timed as the gate cells; the two "
+                          "all-reduces per layer that tensor parallelism adds are not run on one GPU "
+                          "(allreduce_bytes_per_layer: their bf16 payload)",
         "latency_profile": profile,
         "latency_model": latency_model,
         "model_iteration": model,

@@ -54,7 +54,24 @@ class LayerShape:
 TINY = LayerShape("tiny", 256, 4, 2, 64, 688, weight_seed=101)
 LLAMA3_8B = LayerShape("llama3-8b", 4096, 32, 8, 128, 14336, weight_seed=108)
 LLAMA3_70B = LayerShape("llama3-70b", 8192, 64, 8, 128, 28672, weight_seed=170)
-SHAPES = {s.name: s for s in (TINY, LLAMA3_8B, LLAMA3_70B)}
+
+
+def tp_shard(shape: LayerShape, tp: int, weight_seed: int) -> LayerShape:
+    """One GPU's share of a layer under tensor parallelism of degree tp,
+    sharded by heads: n_q/tp query heads, n_kv/tp kv heads (at least one) and
+    ffn_dim/tp FFN columns over the full hidden size. Its own weight seed: the
+    shard's weights are a fresh random init, not a slice of the full layer's."""
+    if shape.n_q_heads % tp or shape.ffn_dim % tp or (shape.n_kv_heads % tp and tp % shape.n_kv_heads):
+        raise ValueError(f"{shape.name} does not shard {tp} ways by heads")
+    return dataclasses.replace(shape, name=f"{shape.name}-tp{tp}-shard", n_q_heads=shape.n_q_heads // tp,
+                               n_kv_heads=max(1, shape.n_kv_heads // tp), ffn_dim=shape.ffn_dim // tp,
+                               weight_seed=weight_seed)
+
+
+# the per-GPU shards of the 8B layer at TP2 and the 70B layer at TP8
+LLAMA3_8B_TP2 = tp_shard(LLAMA3_8B, 2, weight_seed=182)
+LLAMA3_70B_TP8 = tp_shard(LLAMA3_70B, 8, weight_seed=178)
+SHAPES = {s.name: s for s in (TINY, LLAMA3_8B, LLAMA3_70B, LLAMA3_8B_TP2, LLAMA3_70B_TP8)}
 
 
 # ----------------------------------------------------------------------------
@@ -247,14 +264,14 @@ def tiny_batch(seed: int = 1) -> Batch:
     return make_batch(TINY, lens, seed, num_blocks=256, label="tiny")
 
 
-def llama8b_batch(seed: int = 2) -> Batch:
-    """8B layer: one 512-token chunk at offset U{0..4096} plus 64 decodes with
-    contexts U{512..4096}."""
+def llama8b_batch(seed: int = 2, shape: LayerShape = LLAMA3_8B) -> Batch:
+    """8B layer (or one of its shards): one 512-token chunk at offset
+    U{0..4096} plus 64 decodes with contexts U{512..4096}."""
     rng = np.random.default_rng([seed, 0])
     off = int(rng.integers(0, 4096, endpoint=True))
     ctx = rng.integers(512, 4096, size=64, endpoint=True)
     lens = [(512, off)] + [(1, int(c)) for c in ctx]
-    return make_batch(LLAMA3_8B, lens, seed, label="llama3-8b: chunk 512 + 64 decodes")
+    return make_batch(shape, lens, seed, label=f"{shape.name}: chunk 512 + 64 decodes")
 
 
 SWEEP_CHUNKS = (128, 256, 512, 1024, 2048)
@@ -296,10 +313,11 @@ def multi_batch(seed: int = 4) -> Batch:
     return make_batch(LLAMA3_8B, lens, seed, label="llama3-8b: 4 chunks + 256 decodes")
 
 
-def llama70b_batch(seed: int = 5) -> Batch:
-    """70B layer: one 2048-token chunk at offset 30720 plus 32 decodes at context 32768."""
+def llama70b_batch(seed: int = 5, shape: LayerShape = LLAMA3_70B) -> Batch:
+    """70B layer (or one of its shards): one 2048-token chunk at offset 30720
+    plus 32 decodes at context 32768."""
     lens = [(2048, 30720)] + [(1, 32768)] * 32
-    return make_batch(LLAMA3_70B, lens, seed, label="llama3-70b: chunk 2048 + 32 decodes")
+    return make_batch(shape, lens, seed, label=f"{shape.name}: chunk 2048 + 32 decodes")
 
 
 WORKLOADS = {

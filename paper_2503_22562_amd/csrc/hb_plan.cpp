@@ -191,13 +191,24 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p,
   // items about two wave slots' worth of keys per wave (4 per compute unit),
   // at least 1024 keys, so a merged unit spans up to 4 S_i keys and most
   // decodes need no merge kernel. When both kinds are present, tiles run
-  // beside the bandwidth-bound items for the whole launch, so they are split
-  // less (4096 keys). Measured on MI355X over chunk/decode mixes (item split
-  // 512 .. 4096, tile split 1024 .. 4096).
+  // beside the bandwidth-bound items, and a tile is split only as far as it
+  // would otherwise outlast the launch: the launch takes about the longer of
+  // the items' K/V bytes at the HBM rate and the tile steps spread over the
+  // workgroup slots (two per compute unit), and a tile step of 32 keys
+  // (beside an item workgroup) takes about kMixedStepUs. Measured on MI355X
+  // over chunk/decode mixes of the 8B and 70B layers and of their
+  // tensor-parallel shards (item split 256 .. 4096, tile split 1024 .. 16384).
+  constexpr double kMixedStepUs = 0.6, kItemBytesPerUs = 6.0e6;
   const int cus = std::max(1, cu_count);
   const bool mixed = tile_keys > 0 && item_keys > 0;
-  const int S_t = opt.split_tile > 0 ? round_up(opt.split_tile, 64)
-                                     : std::max(mixed ? 4096 : 1024, round_up((int64_t)(tile_keys / (1.0 * cus)) + 1, 64));
+  double s_t = tile_keys / (1.0 * cus);
+  if (mixed) {
+    const double launch_us = std::max(item_keys * 4.0 * d.hd / kItemBytesPerUs,
+                                      tile_keys / 32.0 * kMixedStepUs / (2.0 * cus));
+    s_t = launch_us / kMixedStepUs * 32.0;
+  }
+  const int S_t_auto = std::max(1024, round_up((int64_t)std::min(s_t, 1.0e9) + 1, 64));
+  const int S_t = opt.split_tile > 0 ? round_up(opt.split_tile, 64) : S_t_auto;
   const int S_i = opt.split_item > 0 ? round_up(opt.split_item, 64)
                                      : std::max(1024, round_up((int64_t)(item_keys / (16.0 * cus)) + 1, 64));
   p->split_tile = S_t;
@@ -218,6 +229,10 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p,
   };
   std::vector<AttnItem> merged_items;
   std::vector<Unit> merged_units;
+  struct SplitTile {
+    int first, n, kv_len;  // its pieces are tiles[first .. first + n)
+  };
+  std::vector<SplitTile> split_tiles;
   std::vector<MergeGroup> groups;
   int slots = 0;
   for (int r = 0; r < R; ++r) {
@@ -236,6 +251,7 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p,
             groups.push_back({slots, nspl, kTileCols, tok_start[r] + i0, npos, g, 0, 0});
             slots += nspl * kTileCols;
           }
+          if (nspl > 1) split_tiles.push_back({(int)tiles.size(), nspl, kv_len});
           for (int s = 0; s < nspl; ++s)
             tiles.push_back({r, g, tok_start[r] + i0, x + i0, npos, s * S, std::min(kv_len, (s + 1) * S),
                              nspl > 1 ? part0 + s * kTileCols : -1});
@@ -262,6 +278,23 @@ void build_plan(const Dims& d, const hb_batch_desc* desc, int cu_count, Plan* p,
             merged_items.push_back({r, g, tok_start[r] + i0, x + i0, npos, pb, pe, k > 1 ? part0 + 16 * j : -1});
           }
         }
+      }
+    }
+  }
+  // A split tile is cut at multiples of S_t (full pieces and a shorter
+  // last one). When every work unit gets a workgroup slot of its own (two
+  // per compute unit), nothing queues behind a piece and the launch lasts as
+  // long as the longest one, so the pieces are evened out instead (64-key
+  // multiples, at most S_t; the piece count is unchanged). With more units
+  // than slots, even pieces would add long units to the queue; the short
+  // last pieces fill gaps there.
+  const int64_t item_unit_count = (int64_t)merged_units.size() + ((int64_t)singles.size() + kItemsPerUnit - 1) / kItemsPerUnit;
+  if ((int64_t)tiles.size() + item_unit_count <= 2 * (int64_t)std::max(1, cu_count)) {
+    for (const SplitTile& st : split_tiles) {
+      const int piece = round_up((st.kv_len + st.n - 1) / st.n, 64);
+      for (int s = 0; s < st.n; ++s) {
+        tiles[st.first + s].kv_begin = s * piece;
+        tiles[st.first + s].kv_end = std::min(st.kv_len, (s + 1) * piece);
       }
     }
   }

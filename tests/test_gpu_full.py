@@ -1,4 +1,5 @@
-"""GPU parity at the full Llama-3 8B / 70B layer shapes, in the launch
+"""GPU parity at the full Llama-3 8B / 70B layer shapes and at one GPU's
+share of them under tensor parallelism (8B at TP2, 70B at TP8), in the launch
 configuration the benchmark times, against the fp64 oracle on sampled rows
 (each chunk's first and last rows, random middle rows, random decodes): the
 output y and every intermediate step (q after RoPE, the attention output,
@@ -10,8 +11,9 @@ import numpy as np
 import pytest
 
 import oracle
-from hb_workloads import (LLAMA3_8B, LLAMA3_70B, SWEEP_CHUNKS, SWEEP_DECODES, llama70b_batch, llama8b_batch,
-                          make_weights, multi_batch, sweep_batch, sweep_decode_contexts)
+from hb_workloads import (LLAMA3_8B, LLAMA3_8B_TP2, LLAMA3_70B, LLAMA3_70B_TP8, SWEEP_CHUNKS, SWEEP_DECODES,
+                          llama70b_batch, llama8b_batch, make_weights, multi_batch, sweep_batch,
+                          sweep_decode_contexts)
 from hbref import (assert_parity, assert_stage, assert_swiglu_stage, check_attention_kernel, errors,
                     oracle_for_batch, sample_rows)
 
@@ -115,6 +117,21 @@ def test_latency_profile_monotone_in_chunk_size(hb):
 @pytest.mark.timeout(900)
 def test_llama70b_chunk2048_plus_32_decodes(hb):
     _check_batch(llama70b_batch(), max_T=2080, max_R=64, n_dec=4)
+
+
+@pytest.mark.timeout(900)
+def test_llama70b_tp8_shard_chunk2048_plus_32_decodes(hb):
+    """One GPU's share of the 70B layer under tensor parallelism 8 (8 q heads
+    over one kv head, F 3584, full hidden size) on the 70B request mix: the
+    per-shard GEMM shapes (QKV N = 1280, O K = 1024, gate/up N = 7168, down
+    K = 3584) and attention with eight query heads per kv head."""
+    _check_batch(llama70b_batch(shape=LLAMA3_70B_TP8), max_T=2080, max_R=64, n_dec=4)
+
+
+def test_llama8b_tp2_shard_chunk512_plus_64_decodes(hb):
+    """One GPU's share of the 8B layer under tensor parallelism 2 (16 q / 4
+    kv heads, F 7168) on the bench batch's request mix."""
+    _check_batch(llama8b_batch(shape=LLAMA3_8B_TP2))
 
 
 def _fill_pool_random(dl, seed=5):

@@ -110,7 +110,8 @@ def check(plan, shape, reqs):
 
 
 SHAPES = {"tiny": (256, 4, 2, 64, 688), "8b": (4096, 32, 8, 128, 14336), "70b": (8192, 64, 8, 128, 28672),
-          "g16": (1024, 16, 1, 64, 512), "g1": (512, 4, 4, 128, 336)}
+          "g16": (1024, 16, 1, 64, 512), "g1": (512, 4, 4, 128, 336),
+          "8b-tp2": (4096, 16, 4, 128, 7168), "70b-tp8": (8192, 8, 1, 128, 3584)}
 
 
 @pytest.mark.parametrize("name,reqs,cu", [
@@ -119,6 +120,8 @@ SHAPES = {"tiny": (256, 4, 2, 64, 688), "8b": (4096, 32, 8, 128, 14336), "70b": 
     ("8b", [(2048, 0)], 256),
     ("8b", [(128, 0)] + [(1, int(c)) for c in np.geomspace(256, 8192, 256)], 256),
     ("70b", [(2048, 30720)] + [(1, 32768)] * 32, 256),
+    ("70b-tp8", [(2048, 30720)] + [(1, 32768)] * 32, 256),
+    ("8b-tp2", [(512, 3431)] + [(1, int(c)) for c in np.linspace(512, 4096, 64)], 256),
     ("g16", [(37, 21), (1, 0), (300, 5), (5, 3)], 8),
     ("g1", [(129, 0), (1, 15), (1, 16), (7, 1000)], 4),
     ("8b", [(33, 0), (32, 40), (31, 1)], 1),
@@ -165,3 +168,41 @@ def test_plan_random_batches(driver):
             check(plan, SHAPES[name], reqs)
         except AssertionError as e:
             raise AssertionError(f"case {case}: {name} cu={cu} split_item={split_item} reqs={reqs}: {e}") from e
+
+
+def _split_tile_pieces(plan):
+    """Key ranges of the split tiles, grouped by (request, kv head, first
+    position): {group: sorted [(kv_begin, kv_end)]}."""
+    groups = defaultdict(list)
+    for req, g, tok0, pos0, npos, kb, ke, part in plan["tile"]:
+        if part >= 0:
+            groups[(req, g, pos0)].append((kb, ke))
+    return {k: sorted(v) for k, v in groups.items()}
+
+
+def test_split_tiles_are_even_when_every_unit_has_a_slot(driver):
+    """Mixed launch of the 8B layer's TP2 shard (64 tiles, 256 item units on
+    512 workgroup slots): the longest piece of each split tile is as short as
+    the 64-key step grid allows for its piece count, since the longest piece
+    sets the launch's length."""
+    reqs = [(512, 3431)] + [(1, int(c)) for c in np.linspace(512, 4096, 64)]
+    plan = run_plan(driver, SHAPES["8b-tp2"], 256, reqs)
+    check(plan, SHAPES["8b-tp2"], reqs)
+    pieces = _split_tile_pieces(plan)
+    assert pieces, "no tile was split"
+    for k, v in pieces.items():
+        kv, n = v[-1][1], len(v)
+        assert max(e - b for b, e in v) == -(-(-(-kv // n)) // 64) * 64, (k, v)
+
+
+def test_split_tiles_keep_full_pieces_when_units_queue(driver):
+    """Mixed launch of the 70B layer's TP8 shard (more units than slots):
+    every piece of a split tile but the last spans exactly the split length."""
+    reqs = [(2048, 30720)] + [(1, 32768)] * 32
+    plan = run_plan(driver, SHAPES["70b-tp8"], 256, reqs)
+    check(plan, SHAPES["70b-tp8"], reqs)
+    S = plan["T"][0][1]
+    pieces = _split_tile_pieces(plan)
+    assert pieces, "no tile was split"
+    for k, v in pieces.items():
+        assert all(e - b == S for b, e in v[:-1]) and 0 < v[-1][1] - v[-1][0] <= S, (k, S, v)
