@@ -208,7 +208,9 @@ typedef struct {
  * its batch untimed for 100 ms of device time, so that the GPU is at its
  * steady clocks), run `warmup` untimed
  * iterations, then `iters` iterations each preceded by a write of a 512 MiB
- * buffer (so no data stays in the 256 MB Infinity Cache) and timed with HIP
+ * buffer (so no data stays in the 256 MB Infinity Cache) and a read of
+ * another 512 MiB (so that no written line is left dirty: their write-back
+ * would otherwise fall into the timed iteration), and timed with HIP
  * events; each timed iteration is planned and its metadata uploaded before
  * its start event, so the interval holds the layer's kernels alone.
  * out[m * n_chunk + c] receives the cell. Synchronous. Overwrites the
@@ -222,7 +224,7 @@ hb_status hb_profile(hb_layer* layer, const int32_t* chunk_sizes, int32_t n_chun
 /* Latency of given batches, timed as hb_profile times its cells (the first
  * batch first run untimed for 100 ms of device time): for each
  * batch, `warmup` untimed iterations, then `iters` iterations each after a
- * write of a 512 MiB buffer, each planned and its metadata uploaded before
+ * write of a 512 MiB buffer and a read of another 512 MiB, each planned and its metadata uploaded before
  * the start event, so an interval holds the layer's kernels alone. The
  * caller supplies each batch's inputs, outputs and block tables (and the
  * pool contents); the iterations write the batch's new K/V as

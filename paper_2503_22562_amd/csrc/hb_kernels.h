@@ -131,6 +131,10 @@ void launch_fill_random_bf16(hipStream_t s, uint16_t* p, int64_t n, uint64_t see
 void launch_fill_blocks(hipStream_t s, const int32_t* blocks, int n, int nkv, int hd, uint16_t* k_pool,
                         uint16_t* v_pool, uint64_t seed);
 // Overwrite a buffer (evicts earlier data from the Infinity Cache).
+// Cold-cache preparation over buf[0, bytes): the first half is overwritten
+// with `value`, then the second half is read, so that the caches hold no data
+// of the caller's and none of the written lines are left dirty (their
+// write-back would otherwise fall into whatever runs next).
 void launch_flush(hipStream_t s, void* buf, int64_t bytes, uint32_t value);
 
 // Sustained-rate probes (k_probe.hip): waves reading random 4-KB chunks of

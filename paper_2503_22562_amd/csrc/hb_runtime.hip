@@ -486,9 +486,12 @@ hb_status settle_device(hb_layer* L, const hb_batch_desc* desc, hipEvent_t e0, h
 }
 
 // Time one batch as the profiler does: `warmup` untimed iterations, then
-// `iters` iterations, each after a write of `flush_bytes` (no data left in
-// the Infinity Cache); the batch is planned and its metadata uploaded before
-// the start event, so the interval holds the kernels alone. Fills the cell.
+// `iters` iterations, each after a write of the first half of the
+// `flush_bytes` buffer (no data left in the 256 MB Infinity Cache) and a
+// read of its second half (which evicts the written lines, so that their
+// write-back does not fall into the timed interval); the batch is planned
+// and its metadata uploaded before the start event, so the interval holds
+// the kernels alone. Fills the cell.
 hb_status time_batch(hb_layer* L, const hb_batch_desc* desc, int warmup, int iters, void* flush,
                      int64_t flush_bytes, std::vector<hipEvent_t>& ev, std::vector<float>& lat, hb_profile_cell* cell) {
   hb_status st = check_batch(L->d, L->pool.num_blocks, desc, &L->marks);
@@ -894,7 +897,7 @@ hb_status hb_profile(hb_layer* L, const int32_t* chunk_sizes, int32_t n_chunk, c
   int max_dec = 0;
   for (int mi = 0; mi < n_mix; ++mi) max_dec = std::max(max_dec, mixes[mi].n_decode);
   const int64_t maxT = (int64_t)max_c + max_dec;
-  const int64_t flush_bytes = (int64_t)512 << 20;
+  const int64_t flush_bytes = (int64_t)1 << 30;  // 512 MiB written, 512 MiB read
   void *x_in = nullptr, *x_out = nullptr, *flush = nullptr;
   int32_t* blocks_dev = nullptr;
   std::vector<hipEvent_t> ev;
@@ -961,7 +964,7 @@ hb_status hb_profile_batches(hb_layer* L, const hb_batch_desc* batches, int32_t 
     if (st != HB_OK) return st;
     if (batches[b].n_requests == 0) return fail(HB_ERR_INVALID, "batch %d is empty", b);
   }
-  const int64_t flush_bytes = (int64_t)512 << 20;
+  const int64_t flush_bytes = (int64_t)1 << 30;  // 512 MiB written, 512 MiB read
   void* flush = nullptr;
   std::vector<hipEvent_t> ev(2 * (size_t)iters, nullptr);
   std::vector<float> lat(iters);

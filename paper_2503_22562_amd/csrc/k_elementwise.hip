@@ -159,10 +159,21 @@ __global__ void flush_kernel(u32x4* p, int64_t n, uint32_t value) {
     p[i] = v;
 }
 
+// Grid-stride read of p[0, n); the XOR of the data is stored to *sink only in
+// the (never expected) case that it equals a marker, which keeps the loads.
+__global__ void flush_read_kernel(const u32x4* __restrict__ p, int64_t n, uint32_t* sink) {
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    acc ^= p[i];
+  if ((acc[0] ^ acc[1] ^ acc[2] ^ acc[3]) == 0x5EED5EEDu) *sink = acc[0];
+}
+
 void launch_flush(hipStream_t s, void* buf, int64_t bytes, uint32_t value) {
-  const int64_t n = bytes / 16;
+  const int64_t n = bytes / 32;  // 16-byte elements per half
   if (n <= 0) return;
-  flush_kernel<<<4096, 256, 0, s>>>(reinterpret_cast<u32x4*>(buf), n, value);
+  u32x4* p = reinterpret_cast<u32x4*>(buf);
+  flush_kernel<<<4096, 256, 0, s>>>(p, n, value);
+  flush_read_kernel<<<4096, 256, 0, s>>>(p + n, n, reinterpret_cast<uint32_t*>(buf));
 }
 
 // out[r] = src[rows[r]] for r < n_rows, H bf16 each (H % 8 == 0): token
