@@ -17,6 +17,23 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const void* __restrict__ x
                                                       uint16_t* __restrict__ out, int H, float eps, RopePrep rp) {
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x;
+  const int nvec = H >> 3;
+  // the row's loads are issued first; the RoPE work below runs while they
+  // are in flight
+  u32x4 raw[MAXV][F32IN ? 2 : 1];
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int vi = tid + 256 * i;
+    if (vi < nvec) {
+      if (F32IN) {
+        const float* xr = reinterpret_cast<const float*>(x) + (size_t)row * H + 8 * vi;
+        raw[i][0] = ld16(xr);
+        raw[i][F32IN ? 1 : 0] = ld16(xr + 4);
+      } else {
+        raw[i][0] = ld16(reinterpret_cast<const uint16_t*>(x) + (size_t)row * H + 8 * vi);
+      }
+    }
+  }
   if (ROPE) {
     const int p = rp.tok_pos[row];
     const int half = rp.hd >> 1;
@@ -32,7 +49,6 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const void* __restrict__ x
       rp.slot[row] = blk * 16 + (p & 15);
     }
   }
-  const int nvec = H >> 3;
   float v[MAXV][8];
   float ss = 0.f;
 #pragma unroll
@@ -40,13 +56,12 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const void* __restrict__ x
     const int vi = tid + 256 * i;
     if (vi < nvec) {
       if (F32IN) {
-        const float* xr = reinterpret_cast<const float*>(x) + (size_t)row * H + 8 * vi;
-        u32x4 a = ld16(xr), b = ld16(xr + 4);
-        for (int j = 0; j < 4; ++j) { v[i][j] = __uint_as_float(a[j]); v[i][4 + j] = __uint_as_float(b[j]); }
+        for (int j = 0; j < 4; ++j) {
+          v[i][j] = __uint_as_float(raw[i][0][j]);
+          v[i][4 + j] = __uint_as_float(raw[i][F32IN ? 1 : 0][j]);
+        }
       } else {
-        const uint16_t* xr = reinterpret_cast<const uint16_t*>(x) + (size_t)row * H + 8 * vi;
-        u32x4 a = ld16(xr);
-        for (int j = 0; j < 4; ++j) { v[i][2 * j] = bf16_lo(a[j]); v[i][2 * j + 1] = bf16_hi(a[j]); }
+        for (int j = 0; j < 4; ++j) { v[i][2 * j] = bf16_lo(raw[i][0][j]); v[i][2 * j + 1] = bf16_hi(raw[i][0][j]); }
       }
 #pragma unroll
       for (int j = 0; j < 8; ++j) ss += v[i][j] * v[i][j];
