@@ -130,7 +130,9 @@ def test_llama70b_tp8_shard_chunk2048_plus_32_decodes(hb):
 
 def test_llama8b_tp2_shard_chunk512_plus_64_decodes(hb):
     """One GPU's share of the 8B layer under tensor parallelism 2 (16 q / 4
-    kv heads, F 7168) on the bench batch's request mix."""
+    kv heads, F 7168) on the bench batch's request mix (its split chunk
+    tiles are cut into even pieces: every work unit has a slot; the 70B TP8
+    shard's keep full pieces)."""
     _check_batch(llama8b_batch(shape=LLAMA3_8B_TP2))
 
 
